@@ -1,0 +1,213 @@
+/*
+ * libsd: batched speculative-decoding hot path on one MI355X (gfx950).
+ *
+ * One decoding step of the paper (arXiv 2510.11331, Section II-A, "Inference
+ * Mechanism with SD") for a batch of B tasks:
+ *
+ *   sd_draft_step x gamma   the draft model generates gamma tokens per task
+ *                           autoregressively (drafting phase), each with its
+ *                           draft distribution q;
+ *   sd_verify               the target ("verify") model scores the current
+ *                           input plus the gamma drafts of every task in one
+ *                           forward pass, giving p at gamma+1 positions;
+ *   sd_accept_resample      draft i is accepted with probability
+ *                           min(1, p/q); at the first rejection a correction
+ *                           token is drawn from norm(max(0, p - q)); if all
+ *                           are accepted a reward token is drawn from p;
+ *   sd_kv_commit            rejected drafts are removed from both KV caches
+ *                           and the bonus token becomes the next input.
+ *
+ * The tasks of the paper's problem statement are {I_k, O_k} pairs (input
+ * length, output budget; Section II); here each task lives in a "slot" that
+ * owns paged KV blocks in the target and draft caches.  Section II-B's
+ * pipeline (drafting of one batch overlapping verification of another) is
+ * obtained by calling the draft and verify entry points of two disjoint slot
+ * batches on two streams.
+ *
+ * Conventions
+ *   - Device pointers unless stated otherwise.  The caller owns every buffer
+ *     (weights, KV pools, workspace, inputs, outputs); the context borrows
+ *     them and they must outlive it.  libsd never allocates device memory.
+ *   - Streams are hipStream_t values passed as void* (NULL = null stream).
+ *     Every call except sd_init and sd_prefill only enqueues work on the
+ *     given stream and returns; sd_prefill blocks until its work is done.
+ *   - A negative return value is an error (SD_E*).  Argument and state
+ *     errors are detected on the host before anything is enqueued and leave
+ *     the context unchanged.  No C++ exception crosses this interface.
+ *   - Layouts are row-major.  bf16 data is stored as raw 16-bit patterns.
+ *   - Calls that share one context and overlap in time on different streams
+ *     must use disjoint slots, and at most one draft call and one
+ *     verify/accept/commit sequence may be in flight at a time (they use
+ *     separate halves of the workspace).
+ */
+#ifndef SD_H
+#define SD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sd_ctx sd_ctx;   /* opaque, host-side */
+
+enum {
+    SD_OK = 0,
+    SD_EINVAL = -1,   /* bad argument or configuration                  */
+    SD_ENOMEM = -2,   /* KV block pool cannot hold the request          */
+    SD_ESTATE = -3,   /* call not allowed in the slot's current state   */
+    SD_EHIP = -4      /* a HIP runtime call failed                      */
+};
+
+enum { SD_DTYPE_BF16 = 0, SD_DTYPE_F32 = 1 };
+
+/* Decoder-only model (LLaMA layout of the paper's decoder block, eqs. f11,
+ * f21, f31): RMSNorm -> QKV -> rotary embedding -> causal attention over the
+ * KV cache -> output projection + residual -> RMSNorm -> SwiGLU feed-forward
+ * + residual; final RMSNorm and LM head.  dtype is the storage type of the
+ * weights and the KV cache; for bf16 every matrix-product input is rounded
+ * to bf16, accumulations and the residual stream are fp32. */
+typedef struct {
+    int n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
+    int dtype;              /* SD_DTYPE_BF16 or SD_DTYPE_F32                */
+    float rope_theta;       /* rotary base, e.g. 10000                      */
+    float rms_eps;          /* RMSNorm epsilon, e.g. 1e-5                   */
+} sd_model_cfg;
+
+/* Weights of one model, in the model's dtype.  Matrices are [out, in]
+ * (y = x W^T).  The per-layer pointer arrays are host arrays of n_layers
+ * device pointers; sd_init copies them.
+ *   wqkv  [(n_heads + 2 n_kv_heads) head_dim, d_model]: query rows (head
+ *         major), then key rows, then value rows.
+ *   wo    [d_model, n_heads head_dim]
+ *   wgu   [2 d_ffn, d_model]: gate and up rows interleaved in blocks of 16:
+ *         rows 32b..32b+15 are gate rows 16b..16b+15, rows 32b+16..32b+31
+ *         are up rows 16b..16b+15.
+ *   wdown [d_model, d_ffn]
+ *   embed, lm_head [vocab, d_model]; norms [d_model]. */
+typedef struct {
+    const void *embed, *lm_head, *final_norm;
+    const void *const *attn_norm, *const *wqkv, *const *wo;
+    const void *const *ffn_norm, *const *wgu, *const *wdown;
+} sd_weights;
+
+typedef struct {
+    sd_model_cfg target, draft;  /* same vocab                              */
+    int max_slots;          /* task slots                                   */
+    int max_batch;          /* max tasks per draft/verify call              */
+    int gamma_max;          /* max speculation length (1..16)               */
+    int max_ctx;            /* max positions a slot may reach               */
+    int kv_block;           /* tokens per KV block; must be 16              */
+    int kv_blocks_target;   /* blocks in the target pool                    */
+    int kv_blocks_draft;    /* blocks in the draft pool                     */
+    int prefill_rows;       /* rows per prefill chunk (>= 1)                */
+    float temperature;      /* tau > 0: p = softmax(z / tau)                */
+    int greedy;             /* 1: arg-max drafting and verification         */
+    void *kv_pool_target;   /* sd_kv_pool_bytes(cfg, 0) bytes               */
+    void *kv_pool_draft;    /* sd_kv_pool_bytes(cfg, 1) bytes               */
+    void *workspace;        /* sd_workspace_bytes(cfg) bytes                */
+    size_t workspace_bytes;
+} sd_config;
+
+/* Sizes (host-only queries; 0 on an invalid configuration). */
+size_t sd_kv_pool_bytes(const sd_config *cfg, int draft);
+size_t sd_workspace_bytes(const sd_config *cfg);
+
+/* Validate cfg, borrow the buffers, clear the workspace's device state.
+ * On success *out holds a new context. */
+int sd_init(const sd_config *cfg, const sd_weights *target,
+            const sd_weights *draft, sd_ctx **out);
+
+/* Start B tasks: prompt k (host tokens[off_k .. off_k + lens[k]), packed
+ * back to back) goes to slot slots[k] (host).  Allocates KV blocks for
+ * lens[k] + max_new[k] + gamma_max positions, runs both models over
+ * prompt[:-1] (Section II-A, prefill stage; the target runs the same pass
+ * over the prompt) and sets the slot's next input to the last prompt token.
+ * Blocks until done.  SD_ESTATE if a slot is in use, SD_ENOMEM if a pool
+ * is short. */
+int sd_prefill(sd_ctx *ctx, int B, const int32_t *slots, const int32_t *tokens,
+               const int32_t *lens, const int32_t *max_new, void *stream);
+
+/* Free a slot's KV blocks (host-side; the slot can be prefilled again). */
+int sd_release(sd_ctx *ctx, int slot);
+
+/* Drafting, call i of gamma (Section II-A, decoding stage of the draft):
+ * the first call of a step feeds the draft its pending inputs (the previous
+ * bonus token, preceded by the last accepted draft when all gamma were
+ * accepted), call i > 0 feeds draft token i-1.  Writes
+ *   draft_tok[b * gamma + i]       sampled token (int32)
+ *   q[(b * gamma + i) * vocab ..]  q = softmax(z / tau) (fp32), or the draft
+ *                                  logits in greedy mode.
+ * slots [B] int32; u [B, 2 gamma + 1] uint32 uniforms of this step (column
+ * i is used). */
+int sd_draft_step(sd_ctx *ctx, int B, const int32_t *slots, int gamma, int i,
+                  const uint32_t *u, int32_t *draft_tok, float *q, void *stream);
+
+/* Verification (Section II-A, verification phase): one target forward over
+ * rows b * (gamma+1) + j = [x0, t_1..t_gamma] of every task at positions
+ * P_b .. P_b + gamma, appending their K/V to the target cache.  Writes
+ * p [B, gamma+1, vocab] fp32 = softmax(z / tau) (the logits themselves in
+ * greedy mode) and, if logits is not NULL, the raw logits there. */
+int sd_verify(sd_ctx *ctx, int B, const int32_t *slots, int gamma,
+              const int32_t *draft_tok, float *p, float *logits, void *stream);
+
+/* Acceptance and resampling (Section II-A; speculative sampling): for task
+ * b, draft i is accepted iff fl32(u_i * q_i(t_i)) < p_i(t_i) with
+ * u_i = (u[b, gamma + i] >> 8) * 2^-24; a = index of the first rejection
+ * (gamma if none).  The bonus token is drawn with r = u[b, 2 gamma] by the
+ * integer inverse-CDF rule (W_j = floor(w_j 2^40), T = floor(S r / 2^32),
+ * smallest j with prefix sum > T) from max(0, p_a - q_a) (from p_a if that
+ * has no integer mass) when a < gamma, or from p_gamma when a = gamma.  In
+ * greedy mode draft i is accepted iff it is the arg-max of row i of p (the
+ * target logits; lowest index on ties) and the bonus is that arg-max.
+ * Writes n_acc[b] = a and out_tok[b, 0..gamma] = t_1..t_a, bonus, then -1.
+ * Needs no context: q [B, gamma, vocab], p [B, gamma+1, vocab]. */
+int sd_accept_resample(int B, int gamma, int vocab, int greedy,
+                       const int32_t *draft_tok, const float *q, const float *p,
+                       const uint32_t *u, int32_t *n_acc, int32_t *out_tok,
+                       void *stream);
+
+/* Commit (Section II-A: rejected drafts are removed from both KV caches;
+ * the bonus token is the next input): target length P -> P + a + 1, draft
+ * keeps min(a + 1, gamma) of its new entries, next input = bonus token;
+ * after full acceptance the last draft becomes a pending draft input. */
+int sd_kv_commit(sd_ctx *ctx, int B, const int32_t *slots, int gamma,
+                 const int32_t *n_acc, const int32_t *out_tok, void *stream);
+
+/* Copy slot state to out [B, 4] int32 (device): committed target length
+ * P, next input token x0, pending draft input (-1 if none), KV capacity. */
+int sd_slot_state(sd_ctx *ctx, int B, const int32_t *slots, int32_t *out,
+                  void *stream);
+
+/* Device-side error flags (bit 0: a KV write beyond a slot's capacity was
+ * skipped).  Synchronises the stream; clears the flags. */
+int sd_check(sd_ctx *ctx, void *stream, int32_t *flags_out);
+
+/* Kernel timing with HIP events on the launch stream (off by default).
+ * kind: SD_PROF_* below.  sd_profile_read synchronises the recorded events
+ * and returns the number of timed launches and their summed milliseconds;
+ * reading resets the counters. */
+enum {
+    SD_PROF_GEMM_VERIFY_GATEUP = 0,   /* target FFN gate/up GEMM (+SwiGLU)  */
+    SD_PROF_GEMM_VERIFY_ALL = 1,      /* every target GEMM in sd_verify     */
+    SD_PROF_ATTN_VERIFY = 2,          /* target attention in sd_verify      */
+    SD_PROF_VERIFY = 3,               /* whole sd_verify                    */
+    SD_PROF_DRAFT = 4,                /* whole sd_draft_step                */
+    SD_PROF_N = 5
+};
+int sd_profile(sd_ctx *ctx, int enable);
+int sd_profile_read(sd_ctx *ctx, int kind, int64_t *count, double *ms,
+                    double *bytes);
+
+void sd_destroy(sd_ctx *ctx);
+const char *sd_strerror(int code);
+
+/* Text of the last SD_EHIP failure on the calling thread (HIP call and
+ * message); "" if none.  The string stays valid until the next call. */
+const char *sd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SD_H */

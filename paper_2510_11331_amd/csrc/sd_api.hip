@@ -1,0 +1,803 @@
+// libsd host runtime: configuration checks, workspace layout, the host KV
+// block allocator, and the launch sequences of the prefill, draft and verify
+// passes and of the acceptance / commit step.  See include/sd.h.
+#include "sd.h"
+#include "sd_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <deque>
+#include <new>
+#include <vector>
+
+namespace sd {
+size_t attention_lds_bytes(int hd, int esz, int qmax);
+}
+
+using namespace sd;
+
+namespace {
+
+constexpr int KV_BLOCK = 16;
+constexpr int MAX_SPLITS = 8;
+
+struct ModelRT {
+  sd_model_cfg c{};
+  size_t esz = 2;
+  const void *embed = nullptr, *lm_head = nullptr, *final_norm = nullptr;
+  std::vector<const void*> attn_norm, wqkv, wo, ffn_norm, wgu, wdown;
+  unsigned char* pool = nullptr;
+  int n_blocks = 0;
+  size_t layer_bytes = 0;   // bytes of one layer's pool
+  int nqkv() const { return (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; }
+  int nq() const { return c.n_heads * c.head_dim; }
+  int G() const { return c.n_heads / c.n_kv_heads; }
+};
+
+struct Lane {
+  int rows = 0;                 // row capacity
+  int32_t *row_tok = nullptr, *row_pos = nullptr, *row_slot = nullptr, *rowblocks = nullptr;
+  int rb_cap = 0;
+  float *x = nullptr, *qkv = nullptr, *q = nullptr, *logits = nullptr;
+  void *xn = nullptr, *att = nullptr, *hmid = nullptr;
+  float* partial = nullptr;
+  size_t partial_cap = 0;       // floats
+  int* gemm_cnt = nullptr;
+  int gemm_cnt_n = 0;
+  float *attn_o = nullptr, *attn_ml = nullptr;
+  size_t attn_o_cap = 0, attn_ml_cap = 0;
+  int* attn_cnt = nullptr;
+  int attn_cnt_n = 0;
+};
+
+struct Slot {
+  bool active = false;
+  std::vector<int> tblocks, dblocks;
+};
+
+struct ProfRec {
+  int kind;
+  hipEvent_t a, b;
+  double bytes;
+};
+
+}  // namespace
+
+struct sd_ctx {
+  sd_config cfg{};
+  ModelRT tgt, dft;
+  int mbps = 0;                 // max blocks per slot
+  int32_t *state = nullptr, *bt_t = nullptr, *bt_d = nullptr, *err = nullptr;
+  Lane lv, ld;                  // verify / prefill lane, draft lane
+  int keys_per_split = 64, attn_splits = 1;
+  std::vector<Slot> slots;
+  std::vector<int> free_t, free_d;
+  bool prof = false;
+  std::vector<ProfRec> recs;
+  std::vector<ProfRec> done;
+};
+
+namespace {
+
+thread_local char g_last_error[320] = "";
+
+int hip_fail(hipError_t e, const char* what, int line) {
+  snprintf(g_last_error, sizeof(g_last_error), "sd_api.hip:%d %s: %s", line, what, hipGetErrorString(e));
+  return SD_EHIP;
+}
+
+#define HIPCHK(x)                                                  \
+  do {                                                             \
+    hipError_t e_ = (x);                                           \
+    if (e_ != hipSuccess) return hip_fail(e_, #x, __LINE__);       \
+  } while (0)
+
+size_t esize(int dtype) { return dtype == SD_DTYPE_F32 ? 4 : 2; }
+
+bool model_ok(const sd_model_cfg& m) {
+  if (m.n_layers < 1 || m.d_model < 1 || m.n_heads < 1 || m.n_kv_heads < 1 || m.d_ffn < 1 || m.vocab < 1)
+    return false;
+  if (m.dtype != SD_DTYPE_BF16 && m.dtype != SD_DTYPE_F32) return false;
+  if (m.head_dim != 64 && m.head_dim != 128) return false;
+  if (m.n_heads * m.head_dim != m.d_model) return false;
+  if (m.n_heads % m.n_kv_heads) return false;
+  if ((m.n_heads / m.n_kv_heads) * 2 > ATTN_QMAX) return false;
+  const size_t e = esize(m.dtype);
+  // GEMM K dims stream in 256-byte chunks; N dims come in 16-column tiles
+  if ((m.d_model * e) % GEMM_CHUNK || (m.d_ffn * e) % GEMM_CHUNK) return false;
+  if (m.vocab % 16 || m.d_ffn % 16) return false;
+  if (!(m.rope_theta > 0.f) || !(m.rms_eps > 0.f)) return false;
+  return true;
+}
+
+bool cfg_ok(const sd_config* c) {
+  if (!c) return false;
+  if (!model_ok(c->target) || !model_ok(c->draft)) return false;
+  if (c->target.vocab != c->draft.vocab) return false;
+  if (c->max_slots < 1 || c->max_batch < 1 || c->max_batch > c->max_slots) return false;
+  if (c->gamma_max < 1 || c->gamma_max > 16) return false;
+  if (c->kv_block != KV_BLOCK) return false;
+  if (c->max_ctx < 2 || c->kv_blocks_target < 1 || c->kv_blocks_draft < 1) return false;
+  if (c->prefill_rows < 1) return false;
+  if (!(c->temperature > 0.f)) return false;
+  if ((c->target.n_heads / c->target.n_kv_heads) * (c->gamma_max + 1) > ATTN_QMAX) return false;
+  return true;
+}
+
+size_t pool_bytes(const sd_model_cfg& m, int blocks) {
+  return (size_t)m.n_layers * blocks * 2 * m.n_kv_heads * KV_BLOCK * m.head_dim * esize(m.dtype);
+}
+
+int keys_per_split(int max_ctx) {
+  // aim for at most 12 key splits per (row block, kv head)
+  const int chunks = (max_ctx + 63) / 64;
+  const int per = std::max(1, (chunks + 11) / 12);
+  return per * 64;
+}
+
+struct Alloc {
+  unsigned char* base;   // null: size only
+  size_t off = 0;
+  template <typename P>
+  P* take(size_t bytes) {
+    off = (off + 255) & ~(size_t)255;
+    P* r = base ? (P*)(base + off) : nullptr;
+    off += bytes;
+    return r;
+  }
+};
+
+struct Dims {
+  int d = 0, nqkv = 0, nq = 0, F = 0, V = 0, KV = 0, hd = 0, G = 1;
+  size_t esz = 2;
+};
+
+Dims dims_max(const sd_model_cfg& a, const sd_model_cfg* b) {
+  Dims r;
+  auto upd = [&](const sd_model_cfg& m) {
+    r.d = std::max(r.d, m.d_model);
+    r.nqkv = std::max(r.nqkv, (m.n_heads + 2 * m.n_kv_heads) * m.head_dim);
+    r.nq = std::max(r.nq, m.n_heads * m.head_dim);
+    r.F = std::max(r.F, m.d_ffn);
+    r.V = std::max(r.V, m.vocab);
+    r.KV = std::max(r.KV, m.n_kv_heads);
+    r.hd = std::max(r.hd, m.head_dim);
+    r.G = std::max(r.G, m.n_heads / m.n_kv_heads);
+    r.esz = std::max(r.esz, esize(m.dtype));
+  };
+  upd(a);
+  if (b) upd(*b);
+  return r;
+}
+
+// lane buffers; decode_rb = row blocks of a decode pass, qmax_dec = query vectors per row block
+void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int qmax_dec, int splits,
+              int logits_rows, int prefill_rb) {
+  ln.rows = rows;
+  ln.row_tok = al.take<int32_t>(sizeof(int32_t) * rows);
+  ln.row_pos = al.take<int32_t>(sizeof(int32_t) * rows);
+  ln.row_slot = al.take<int32_t>(sizeof(int32_t) * rows);
+  ln.rb_cap = prefill_rb;
+  ln.rowblocks = al.take<int32_t>(sizeof(int32_t) * 2 * std::max(1, prefill_rb));
+  ln.x = al.take<float>(sizeof(float) * rows * D.d);
+  ln.xn = al.take<void>(D.esz * rows * D.d);
+  ln.qkv = al.take<float>(sizeof(float) * rows * D.nqkv);
+  ln.q = al.take<float>(sizeof(float) * rows * D.nq);
+  ln.att = al.take<void>(D.esz * rows * D.nq);
+  ln.hmid = al.take<void>(D.esz * rows * D.F);
+  ln.logits = logits_rows ? al.take<float>(sizeof(float) * logits_rows * D.V) : nullptr;
+  const int nmax = std::max(std::max(D.nqkv, D.d), std::max(2 * D.F, D.V));
+  ln.partial_cap = (size_t)MAX_SPLITS * std::min(rows, GEMM_MROWS) * nmax;
+  ln.partial = al.take<float>(sizeof(float) * ln.partial_cap);
+  ln.gemm_cnt_n = (nmax + 63) / 64 + 1;
+  ln.gemm_cnt = al.take<int>(sizeof(int) * ln.gemm_cnt_n);
+  ln.attn_cnt_n = decode_rb * D.KV;
+  ln.attn_o_cap = (size_t)ln.attn_cnt_n * splits * qmax_dec * D.hd;
+  ln.attn_ml_cap = (size_t)ln.attn_cnt_n * splits * qmax_dec * 2;
+  ln.attn_o = al.take<float>(sizeof(float) * ln.attn_o_cap);
+  ln.attn_ml = al.take<float>(sizeof(float) * ln.attn_ml_cap);
+  ln.attn_cnt = al.take<int>(sizeof(int) * std::max(1, ln.attn_cnt_n));
+}
+
+// prefill rows per attention row block: as many as fit the 64 query vectors
+// of a workgroup and the default 64 KB of dynamic LDS
+int prefill_qb(const sd_model_cfg& m) {
+  const int G = m.n_heads / m.n_kv_heads;
+  int qb = std::max(1, ATTN_QMAX / G);
+  while (qb > 1 && attention_lds_bytes(m.head_dim, esize(m.dtype), qb * G) > 64 * 1024) --qb;
+  return qb;
+}
+
+size_t layout(const sd_config* c, sd_ctx* ctx) {
+  Alloc al{ctx ? (unsigned char*)c->workspace : nullptr};
+  const int mbps = (c->max_ctx + KV_BLOCK - 1) / KV_BLOCK;
+  int32_t* state = al.take<int32_t>(sizeof(int32_t) * ST_N * c->max_slots);
+  int32_t* bt_t = al.take<int32_t>(sizeof(int32_t) * (size_t)c->max_slots * mbps);
+  int32_t* bt_d = al.take<int32_t>(sizeof(int32_t) * (size_t)c->max_slots * mbps);
+  int32_t* err = al.take<int32_t>(sizeof(int32_t) * 4);
+  const int kps = keys_per_split(c->max_ctx);
+  const int splits = (c->max_ctx + kps - 1) / kps;
+  const Dims Dt = dims_max(c->target, &c->draft);
+  const Dims Dd = dims_max(c->draft, nullptr);
+  const int rows_v = std::max(c->max_batch * (c->gamma_max + 1), c->prefill_rows);
+  const int qb = std::min(prefill_qb(c->target), prefill_qb(c->draft));
+  const int prefill_rb = c->prefill_rows / qb + c->max_slots + 1;
+  Lane lv, ld;
+  lay_lane(al, lv, rows_v, Dt, c->max_batch, (c->gamma_max + 1) * Dt.G, splits, 0, prefill_rb);
+  lay_lane(al, ld, 2 * c->max_batch, Dd, c->max_batch, 2 * Dd.G, splits, c->max_batch, 0);
+  if (ctx) {
+    ctx->mbps = mbps;
+    ctx->state = state;
+    ctx->bt_t = bt_t;
+    ctx->bt_d = bt_d;
+    ctx->err = err;
+    ctx->lv = lv;
+    ctx->ld = ld;
+    ctx->keys_per_split = kps;
+    ctx->attn_splits = splits;
+  }
+  return (al.off + 255) & ~(size_t)255;
+}
+
+// ---------------------------------------------------------------- profiling
+
+void prof_begin(sd_ctx* ctx, hipStream_t s, ProfRec& r, int kind, double bytes) {
+  r.kind = -1;
+  if (!ctx->prof || kind < 0) return;
+  if (hipEventCreate(&r.a) != hipSuccess) return;
+  if (hipEventCreate(&r.b) != hipSuccess) { hipEventDestroy(r.a); return; }
+  if (hipEventRecord(r.a, s) != hipSuccess) { hipEventDestroy(r.a); hipEventDestroy(r.b); return; }
+  r.kind = kind;
+  r.bytes = bytes;
+}
+void prof_end(sd_ctx* ctx, hipStream_t s, ProfRec& r) {
+  if (r.kind < 0) return;
+  hipEventRecord(r.b, s);
+  ctx->recs.push_back(r);
+}
+
+// ---------------------------------------------------------------- GEMM planning
+
+struct GemmPlan {
+  int mt, gx, gz, splits, cps;
+};
+
+GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, size_t partial_cap) {
+  GemmPlan g{};
+  g.gz = (M + GEMM_MROWS - 1) / GEMM_MROWS;
+  g.mt = g.gz > 1 ? 4 : (M + 15) / 16;
+  g.gx = (N + gemm_cols_per_wg(epi) - 1) / gemm_cols_per_wg(epi);
+  const int chunks = (int)(K * esz / GEMM_CHUNK);
+  int splits = 1;
+  if (g.gz == 1) {
+    const int target_wgs = 512;
+    splits = std::min(std::min(MAX_SPLITS, chunks), std::max(1, (target_wgs + g.gx - 1) / g.gx));
+    while (splits > 1 && (size_t)splits * M * N > partial_cap) --splits;
+  }
+  g.cps = (chunks + splits - 1) / splits;
+  g.splits = (chunks + g.cps - 1) / g.cps;
+  return g;
+}
+
+int gemm(sd_ctx* ctx, Lane& ln, const ModelRT& m, int epi, const void* A, const void* W, int M, int N,
+         int K, float* out, int ldo, void* out_t, hipStream_t s, int prof_kind, int prof_kind2) {
+  const GemmPlan g = plan_gemm(M, N, K, m.esz, epi, ln.partial_cap);
+  if (g.gx + 1 > ln.gemm_cnt_n && g.splits > 1) return SD_EINVAL;
+  GemmParams p{};
+  p.A = A;
+  p.W = W;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.splits = g.splits;
+  p.chunks_per_split = g.cps;
+  p.partial = ln.partial;
+  p.counters = ln.gemm_cnt;
+  p.out = out;
+  p.ldo = ldo;
+  p.out_t = out_t;
+  const double out_bytes = epi == EPI_SWIGLU ? (double)M * (N / 2) * m.esz
+                                             : (double)M * N * 4 * (epi == EPI_RESID ? 2 : 1);
+  const double bytes = (double)N * K * m.esz + (double)M * K * m.esz + out_bytes;
+  ProfRec r1, r2;
+  prof_begin(ctx, s, r1, prof_kind, bytes);
+  prof_begin(ctx, s, r2, prof_kind2, bytes);
+  HIPCHK(launch_gemm(m.c.dtype == SD_DTYPE_F32 ? 1 : 0, epi, g.mt, g.gx, g.gz, p, s));
+  prof_end(ctx, s, r2);
+  prof_end(ctx, s, r1);
+  return SD_OK;
+}
+
+// One forward pass of a model over the rows set up by `rows` (or already in
+// the lane for prefill).  lm_M > 0: final norm over rows r*lm_stride+lm_off
+// and LM head into `logits` [lm_M, V].
+int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, const int32_t* rowblocks,
+            int R, int attn_splits, int qmax, int lm_M, int lm_stride, int lm_off, float* logits,
+            const int32_t* bt, bool verify, hipStream_t s) {
+  const sd_model_cfg& c = m.c;
+  const int dt = c.dtype == SD_DTYPE_F32 ? 1 : 0;
+  const int d = c.d_model;
+  rows.M = M;
+  rows.embed = m.embed;
+  rows.gain = m.attn_norm[0];
+  rows.x = ln.x;
+  rows.xn = ln.xn;
+  rows.d = d;
+  rows.V = c.vocab;
+  rows.eps = c.rms_eps;
+  rows.row_tok = ln.row_tok;
+  rows.row_pos = ln.row_pos;
+  rows.row_slot = ln.row_slot;
+  rows.state = ctx->state;
+  rows.err = ctx->err;
+  rows.n_slots = ctx->cfg.max_slots;
+  HIPCHK(launch_rows_embed(dt, rows, s));
+  const int pk_all = verify ? SD_PROF_GEMM_VERIFY_ALL : -1;
+  for (int l = 0; l < c.n_layers; ++l) {
+    int rc = gemm(ctx, ln, m, EPI_STORE, ln.xn, m.wqkv[l], M, m.nqkv(), d, ln.qkv, m.nqkv(), nullptr, s,
+                  pk_all, -1);
+    if (rc) return rc;
+    RopeParams rp{};
+    rp.qkv = ln.qkv;
+    rp.q = ln.q;
+    rp.kv = m.pool + (size_t)l * m.layer_bytes;
+    rp.row_pos = ln.row_pos;
+    rp.row_slot = ln.row_slot;
+    rp.block_table = bt;
+    rp.state = ctx->state;
+    rp.M = M;
+    rp.H = c.n_heads;
+    rp.KV = c.n_kv_heads;
+    rp.hd = c.head_dim;
+    rp.mbps = ctx->mbps;
+    rp.theta = c.rope_theta;
+    rp.err = ctx->err;
+    HIPCHK(launch_rope_append(dt, rp, s));
+    AttnParams ap{};
+    ap.q = ln.q;
+    ap.kv = rp.kv;
+    ap.block_table = bt;
+    ap.mbps = ctx->mbps;
+    ap.row_pos = ln.row_pos;
+    ap.row_slot = ln.row_slot;
+    ap.rowblocks = rowblocks;
+    ap.R = R;
+    ap.nrb = nrb;
+    ap.H = c.n_heads;
+    ap.KV = c.n_kv_heads;
+    ap.hd = c.head_dim;
+    ap.splits = attn_splits;
+    ap.keys_per_split = attn_splits > 1 ? ctx->keys_per_split : ctx->cfg.max_ctx;
+    ap.scale = 1.0f / sqrtf((float)c.head_dim);
+    ap.out = ln.att;
+    ap.part_o = ln.attn_o;
+    ap.part_ml = ln.attn_ml;
+    ap.counters = ln.attn_cnt;
+    ap.qmax = qmax;
+    ProfRec ra;
+    prof_begin(ctx, s, ra, verify ? SD_PROF_ATTN_VERIFY : -1, 0);
+    HIPCHK(launch_attention(dt, ap, s));
+    prof_end(ctx, s, ra);
+    rc = gemm(ctx, ln, m, EPI_RESID, ln.att, m.wo[l], M, d, m.nq(), ln.x, d, nullptr, s, pk_all, -1);
+    if (rc) return rc;
+    NormParams np{ln.x, m.ffn_norm[l], ln.xn, M, d, 1, 0, c.rms_eps};
+    HIPCHK(launch_rmsnorm(dt, np, s));
+    rc = gemm(ctx, ln, m, EPI_SWIGLU, ln.xn, m.wgu[l], M, 2 * c.d_ffn, d, nullptr, 0, ln.hmid, s, pk_all,
+              verify ? SD_PROF_GEMM_VERIFY_GATEUP : -1);
+    if (rc) return rc;
+    rc = gemm(ctx, ln, m, EPI_RESID, ln.hmid, m.wdown[l], M, d, c.d_ffn, ln.x, d, nullptr, s, pk_all, -1);
+    if (rc) return rc;
+    if (l + 1 < c.n_layers) {
+      NormParams nn{ln.x, m.attn_norm[l + 1], ln.xn, M, d, 1, 0, c.rms_eps};
+      HIPCHK(launch_rmsnorm(dt, nn, s));
+    }
+  }
+  if (lm_M > 0) {
+    NormParams fn{ln.x, m.final_norm, ln.xn, lm_M, d, lm_stride, lm_off, c.rms_eps};
+    HIPCHK(launch_rmsnorm(dt, fn, s));
+    int rc = gemm(ctx, ln, m, EPI_STORE, ln.xn, m.lm_head, lm_M, c.vocab, d, logits, c.vocab, nullptr, s,
+                  pk_all, -1);
+    if (rc) return rc;
+  }
+  return SD_OK;
+}
+
+bool model_ptrs_ok(const sd_weights* w, int L) {
+  if (!w || !w->embed || !w->lm_head || !w->final_norm) return false;
+  if (!w->attn_norm || !w->wqkv || !w->wo || !w->ffn_norm || !w->wgu || !w->wdown) return false;
+  for (int l = 0; l < L; ++l)
+    if (!w->attn_norm[l] || !w->wqkv[l] || !w->wo[l] || !w->ffn_norm[l] || !w->wgu[l] || !w->wdown[l])
+      return false;
+  return true;
+}
+
+void load_model(ModelRT& m, const sd_model_cfg& c, const sd_weights* w, void* pool, int blocks) {
+  m.c = c;
+  m.esz = esize(c.dtype);
+  m.embed = w->embed;
+  m.lm_head = w->lm_head;
+  m.final_norm = w->final_norm;
+  m.attn_norm.assign(w->attn_norm, w->attn_norm + c.n_layers);
+  m.wqkv.assign(w->wqkv, w->wqkv + c.n_layers);
+  m.wo.assign(w->wo, w->wo + c.n_layers);
+  m.ffn_norm.assign(w->ffn_norm, w->ffn_norm + c.n_layers);
+  m.wgu.assign(w->wgu, w->wgu + c.n_layers);
+  m.wdown.assign(w->wdown, w->wdown + c.n_layers);
+  m.pool = (unsigned char*)pool;
+  m.n_blocks = blocks;
+  m.layer_bytes = pool_bytes(c, blocks) / c.n_layers;
+}
+
+bool batch_ok(sd_ctx* ctx, int B, const void* slots, int gamma) {
+  return ctx && B >= 1 && B <= ctx->cfg.max_batch && slots && gamma >= 1 && gamma <= ctx->cfg.gamma_max;
+}
+
+}  // namespace
+
+// ============================================================== C ABI
+
+extern "C" {
+
+size_t sd_kv_pool_bytes(const sd_config* cfg, int draft) {
+  if (!cfg_ok(cfg)) return 0;
+  return draft ? pool_bytes(cfg->draft, cfg->kv_blocks_draft) : pool_bytes(cfg->target, cfg->kv_blocks_target);
+}
+
+size_t sd_workspace_bytes(const sd_config* cfg) {
+  if (!cfg_ok(cfg)) return 0;
+  return layout(cfg, nullptr);
+}
+
+int sd_init(const sd_config* cfg, const sd_weights* target, const sd_weights* draft, sd_ctx** out) {
+  if (!out) return SD_EINVAL;
+  *out = nullptr;
+  if (!cfg_ok(cfg)) return SD_EINVAL;
+  if (!model_ptrs_ok(target, cfg->target.n_layers) || !model_ptrs_ok(draft, cfg->draft.n_layers))
+    return SD_EINVAL;
+  if (!cfg->kv_pool_target || !cfg->kv_pool_draft || !cfg->workspace) return SD_EINVAL;
+  if (cfg->workspace_bytes < layout(cfg, nullptr)) return SD_EINVAL;
+  if (((uintptr_t)cfg->workspace | (uintptr_t)cfg->kv_pool_target | (uintptr_t)cfg->kv_pool_draft) & 255)
+    return SD_EINVAL;
+  sd_ctx* ctx = new (std::nothrow) sd_ctx();
+  if (!ctx) return SD_EINVAL;
+  ctx->cfg = *cfg;
+  load_model(ctx->tgt, cfg->target, target, cfg->kv_pool_target, cfg->kv_blocks_target);
+  load_model(ctx->dft, cfg->draft, draft, cfg->kv_pool_draft, cfg->kv_blocks_draft);
+  layout(cfg, ctx);
+  ctx->slots.resize(cfg->max_slots);
+  for (int b = cfg->kv_blocks_target - 1; b >= 0; --b) ctx->free_t.push_back(b);
+  for (int b = cfg->kv_blocks_draft - 1; b >= 0; --b) ctx->free_d.push_back(b);
+  // device state: zero counters, invalid slots, no errors (fill kernels, synchronous here)
+  hipStream_t s = nullptr;
+  bool ok = launch_fill_i32((int32_t*)cfg->workspace, 0, layout(cfg, nullptr) / 4, s) == hipSuccess &&
+            hipStreamSynchronize(s) == hipSuccess;
+  if (!ok) {
+    delete ctx;
+    return SD_EHIP;
+  }
+  *out = ctx;
+  return SD_OK;
+}
+
+int sd_prefill(sd_ctx* ctx, int B, const int32_t* slots, const int32_t* tokens, const int32_t* lens,
+               const int32_t* max_new, void* stream) {
+  if (!ctx || B < 1 || !slots || !tokens || !lens || !max_new) return SD_EINVAL;
+  const sd_config& c = ctx->cfg;
+  hipStream_t s = (hipStream_t)stream;
+  std::vector<char> seen(c.max_slots, 0);
+  size_t need_t = 0, need_d = 0;
+  for (int k = 0; k < B; ++k) {
+    if (slots[k] < 0 || slots[k] >= c.max_slots || seen[slots[k]]) return SD_EINVAL;
+    seen[slots[k]] = 1;
+    if (lens[k] < 1 || max_new[k] < 1) return SD_EINVAL;
+    if ((long)lens[k] + max_new[k] + c.gamma_max > c.max_ctx) return SD_EINVAL;
+    if (ctx->slots[slots[k]].active) return SD_ESTATE;
+    const int nb = (lens[k] + max_new[k] + c.gamma_max + KV_BLOCK - 1) / KV_BLOCK;
+    need_t += nb;
+    need_d += nb;
+  }
+  size_t off = 0;
+  for (int k = 0; k < B; ++k) {
+    for (int i = 0; i < lens[k]; ++i)
+      if (tokens[off + i] < 0 || tokens[off + i] >= c.target.vocab) return SD_EINVAL;
+    off += lens[k];
+  }
+  if (need_t > ctx->free_t.size() || need_d > ctx->free_d.size()) return SD_ENOMEM;
+
+  // allocate blocks and build the host images of state and block tables
+  std::vector<int32_t> st(ST_N * B), bt(ctx->mbps * (size_t)B * 2, 0);
+  off = 0;
+  for (int k = 0; k < B; ++k) {
+    Slot& sl = ctx->slots[slots[k]];
+    const int nb = (lens[k] + max_new[k] + c.gamma_max + KV_BLOCK - 1) / KV_BLOCK;
+    sl.tblocks.clear();
+    sl.dblocks.clear();
+    for (int i = 0; i < nb; ++i) {
+      sl.tblocks.push_back(ctx->free_t.back());
+      ctx->free_t.pop_back();
+      sl.dblocks.push_back(ctx->free_d.back());
+      ctx->free_d.pop_back();
+      bt[(size_t)k * ctx->mbps + i] = sl.tblocks[i];
+      bt[(size_t)(B + k) * ctx->mbps + i] = sl.dblocks[i];
+    }
+    st[k * ST_N + ST_LEN] = lens[k] - 1;
+    st[k * ST_N + ST_X0] = tokens[off + lens[k] - 1];
+    st[k * ST_N + ST_PEND] = -1;
+    st[k * ST_N + ST_CAP] = nb * KV_BLOCK;
+    off += lens[k];
+  }
+  auto undo = [&]() {
+    for (int k = 0; k < B; ++k) {
+      Slot& sl = ctx->slots[slots[k]];
+      for (int b : sl.tblocks) ctx->free_t.push_back(b);
+      for (int b : sl.dblocks) ctx->free_d.push_back(b);
+      sl.tblocks.clear();
+      sl.dblocks.clear();
+    }
+  };
+  for (int k = 0; k < B; ++k) {
+    if (hipMemcpyAsync(ctx->state + (size_t)slots[k] * ST_N, &st[k * ST_N], sizeof(int32_t) * ST_N,
+                       hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(ctx->bt_t + (size_t)slots[k] * ctx->mbps, &bt[(size_t)k * ctx->mbps],
+                       sizeof(int32_t) * ctx->mbps, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(ctx->bt_d + (size_t)slots[k] * ctx->mbps, &bt[(size_t)(B + k) * ctx->mbps],
+                       sizeof(int32_t) * ctx->mbps, hipMemcpyHostToDevice, s) != hipSuccess) {
+      undo();
+      return hip_fail(hipGetLastError(), "prefill state upload", __LINE__);
+    }
+  }
+
+  // rows: prompt[:-1] of every task, in chunks of prefill_rows
+  struct RowRec { int32_t tok, pos, slot; };
+  std::vector<RowRec> all;
+  off = 0;
+  for (int k = 0; k < B; ++k) {
+    for (int i = 0; i + 1 < lens[k]; ++i) all.push_back({tokens[off + i], i, slots[k]});
+    off += lens[k];
+  }
+  Lane& ln = ctx->lv;
+  // host staging kept alive until the final synchronize; a deque keeps references stable
+  std::deque<std::vector<int32_t>> keep;
+  int rc = SD_OK;
+  for (size_t c0 = 0; c0 < all.size() && rc == SD_OK; c0 += c.prefill_rows) {
+    const int M = (int)std::min(all.size() - c0, (size_t)c.prefill_rows);
+    keep.emplace_back(3 * (size_t)M);
+    std::vector<int32_t>& rows = keep.back();
+    for (int r = 0; r < M; ++r) {
+      rows[r] = all[c0 + r].tok;
+      rows[M + r] = all[c0 + r].pos;
+      rows[2 * M + r] = all[c0 + r].slot;
+    }
+    if (hipMemcpyAsync(ln.row_tok, rows.data(), sizeof(int32_t) * M, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(ln.row_pos, rows.data() + M, sizeof(int32_t) * M, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(ln.row_slot, rows.data() + 2 * M, sizeof(int32_t) * M, hipMemcpyHostToDevice, s) !=
+            hipSuccess) {
+      rc = hip_fail(hipGetLastError(), "prefill row upload", __LINE__);
+      break;
+    }
+    for (int which = 0; which < 2 && rc == SD_OK; ++which) {
+      ModelRT& m = which == 0 ? ctx->tgt : ctx->dft;
+      const int qb = prefill_qb(m.c);
+      keep.emplace_back();
+      std::vector<int32_t>& rbv = keep.back();
+      for (int r = 0; r < M;) {
+        int e = r + 1;
+        while (e < M && e - r < qb && rows[2 * M + e] == rows[2 * M + r]) ++e;
+        rbv.push_back(r);
+        rbv.push_back(e - r);
+        r = e;
+      }
+      const int nrb = (int)rbv.size() / 2;
+      if (nrb > ln.rb_cap) { rc = SD_EINVAL; break; }
+      // each model's row blocks go to their own half of the row-block buffer region in turn;
+      // the copy is ordered after the previous model's kernels on the same stream
+      if (hipMemcpyAsync(ln.rowblocks, rbv.data(), sizeof(int32_t) * rbv.size(), hipMemcpyHostToDevice, s) !=
+          hipSuccess) {
+        rc = hip_fail(hipGetLastError(), "prefill row-block upload", __LINE__);
+        break;
+      }
+      RowsParams rp{};
+      rp.mode = ROWS_PREFILL;
+      rc = forward(ctx, m, ln, rp, M, nrb, ln.rowblocks, 0, 1, qb * m.G(), 0, 1, 0, nullptr,
+                   which == 0 ? ctx->bt_t : ctx->bt_d, false, s);
+    }
+  }
+  {
+    const hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) rc = hip_fail(e, "prefill synchronize", __LINE__);
+  }
+  if (rc != SD_OK) {
+    undo();
+    return rc;
+  }
+  for (int k = 0; k < B; ++k) ctx->slots[slots[k]].active = true;
+  return SD_OK;
+}
+
+int sd_release(sd_ctx* ctx, int slot) {
+  if (!ctx || slot < 0 || slot >= ctx->cfg.max_slots) return SD_EINVAL;
+  Slot& sl = ctx->slots[slot];
+  if (!sl.active) return SD_ESTATE;
+  for (int b : sl.tblocks) ctx->free_t.push_back(b);
+  for (int b : sl.dblocks) ctx->free_d.push_back(b);
+  sl.tblocks.clear();
+  sl.dblocks.clear();
+  sl.active = false;
+  return SD_OK;
+}
+
+int sd_draft_step(sd_ctx* ctx, int B, const int32_t* slots, int gamma, int i, const uint32_t* u,
+                  int32_t* draft_tok, float* q, void* stream) {
+  if (!batch_ok(ctx, B, slots, gamma) || i < 0 || i >= gamma || !u || !draft_tok || !q) return SD_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  ModelRT& m = ctx->dft;
+  Lane& ln = ctx->ld;
+  const bool first = i == 0;
+  const int R = first ? 2 : 1;
+  const int M = B * R;
+  RowsParams rp{};
+  rp.mode = first ? ROWS_DRAFT_FIRST : ROWS_DRAFT_NEXT;
+  rp.B = B;
+  rp.gamma = gamma;
+  rp.step_i = i;
+  rp.slots = slots;
+  rp.draft_tok = draft_tok;
+  ProfRec pr;
+  prof_begin(ctx, s, pr, SD_PROF_DRAFT, 0);
+  int rc = forward(ctx, m, ln, rp, M, B, nullptr, R, ctx->attn_splits, R * m.G(), B, R, R - 1, ln.logits,
+                   ctx->bt_d, false, s);
+  if (rc) return rc;
+  DraftSampleParams dp{};
+  dp.z = ln.logits;
+  dp.q = q;
+  dp.draft_tok = draft_tok;
+  dp.u = u;
+  dp.B = B;
+  dp.V = m.c.vocab;
+  dp.gamma = gamma;
+  dp.i = i;
+  dp.inv_tau = 1.0f / ctx->cfg.temperature;
+  dp.greedy = ctx->cfg.greedy;
+  HIPCHK(launch_draft_sample(dp, s));
+  prof_end(ctx, s, pr);
+  return SD_OK;
+}
+
+int sd_verify(sd_ctx* ctx, int B, const int32_t* slots, int gamma, const int32_t* draft_tok, float* p,
+              float* logits, void* stream) {
+  if (!batch_ok(ctx, B, slots, gamma) || !draft_tok || !p) return SD_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  ModelRT& m = ctx->tgt;
+  Lane& ln = ctx->lv;
+  const int R = gamma + 1;
+  const int M = B * R;
+  RowsParams rp{};
+  rp.mode = ROWS_VERIFY;
+  rp.B = B;
+  rp.gamma = gamma;
+  rp.slots = slots;
+  rp.draft_tok = draft_tok;
+  float* z = logits ? logits : p;
+  ProfRec pr;
+  prof_begin(ctx, s, pr, SD_PROF_VERIFY, 0);
+  int rc = forward(ctx, m, ln, rp, M, B, nullptr, R, ctx->attn_splits, R * m.G(), M, 1, 0, z, ctx->bt_t,
+                   true, s);
+  if (rc) return rc;
+  SoftmaxParams sp{z, p, M, m.c.vocab, 1.0f / ctx->cfg.temperature, ctx->cfg.greedy};
+  HIPCHK(launch_softmax(sp, s));
+  prof_end(ctx, s, pr);
+  return SD_OK;
+}
+
+int sd_accept_resample(int B, int gamma, int vocab, int greedy, const int32_t* draft_tok, const float* q,
+                       const float* p, const uint32_t* u, int32_t* n_acc, int32_t* out_tok, void* stream) {
+  if (B < 1 || gamma < 1 || gamma > 64 || vocab < 1 || !draft_tok || !q || !p || !u || !n_acc || !out_tok)
+    return SD_EINVAL;
+  AcceptParams ap{};
+  ap.B = B;
+  ap.gamma = gamma;
+  ap.V = vocab;
+  ap.greedy = greedy ? 1 : 0;
+  ap.draft_tok = draft_tok;
+  ap.q = q;
+  ap.p = p;
+  ap.u = u;
+  ap.n_acc = n_acc;
+  ap.out_tok = out_tok;
+  ap.err = nullptr;
+  HIPCHK(launch_accept(ap, (hipStream_t)stream));
+  return SD_OK;
+}
+
+int sd_kv_commit(sd_ctx* ctx, int B, const int32_t* slots, int gamma, const int32_t* n_acc,
+                 const int32_t* out_tok, void* stream) {
+  if (!batch_ok(ctx, B, slots, gamma) || !n_acc || !out_tok) return SD_EINVAL;
+  CommitParams cp{B, gamma, ctx->cfg.max_slots, slots, n_acc, out_tok, ctx->state, ctx->err};
+  HIPCHK(launch_commit(cp, (hipStream_t)stream));
+  return SD_OK;
+}
+
+int sd_slot_state(sd_ctx* ctx, int B, const int32_t* slots, int32_t* out, void* stream) {
+  if (!ctx || B < 1 || !slots || !out) return SD_EINVAL;
+  // gather via the commit-free path: one tiny copy per row on the stream
+  hipStream_t s = (hipStream_t)stream;
+  std::vector<int32_t> hs(B);
+  HIPCHK(hipMemcpyAsync(hs.data(), slots, sizeof(int32_t) * B, hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  for (int b = 0; b < B; ++b) {
+    if (hs[b] < 0 || hs[b] >= ctx->cfg.max_slots) return SD_EINVAL;
+    HIPCHK(hipMemcpyAsync(out + (size_t)b * ST_N, ctx->state + (size_t)hs[b] * ST_N, sizeof(int32_t) * ST_N,
+                          hipMemcpyDeviceToDevice, s));
+  }
+  return SD_OK;
+}
+
+int sd_check(sd_ctx* ctx, void* stream, int32_t* flags_out) {
+  if (!ctx) return SD_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  int32_t f = 0;
+  HIPCHK(hipMemcpyAsync(&f, ctx->err, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  HIPCHK(launch_fill_i32(ctx->err, 0, 1, s));
+  HIPCHK(hipStreamSynchronize(s));
+  if (flags_out) *flags_out = f;
+  return SD_OK;
+}
+
+int sd_profile(sd_ctx* ctx, int enable) {
+  if (!ctx) return SD_EINVAL;
+  ctx->prof = enable != 0;
+  return SD_OK;
+}
+
+int sd_profile_read(sd_ctx* ctx, int kind, int64_t* count, double* ms, double* bytes) {
+  if (!ctx || kind < 0 || kind >= SD_PROF_N) return SD_EINVAL;
+  int64_t n = 0;
+  double t = 0, by = 0;
+  std::vector<ProfRec> keep;
+  for (ProfRec& r : ctx->recs) {
+    if (r.kind != kind) {
+      keep.push_back(r);
+      continue;
+    }
+    float e = 0.f;
+    if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&e, r.a, r.b) == hipSuccess) {
+      ++n;
+      t += e;
+      by += r.bytes;
+    }
+    hipEventDestroy(r.a);
+    hipEventDestroy(r.b);
+  }
+  ctx->recs.swap(keep);
+  if (count) *count = n;
+  if (ms) *ms = t;
+  if (bytes) *bytes = by;
+  return SD_OK;
+}
+
+void sd_destroy(sd_ctx* ctx) {
+  if (!ctx) return;
+  for (ProfRec& r : ctx->recs) {
+    hipEventDestroy(r.a);
+    hipEventDestroy(r.b);
+  }
+  delete ctx;
+}
+
+const char* sd_last_error(void) { return g_last_error; }
+
+const char* sd_strerror(int code) {
+  switch (code) {
+    case SD_OK: return "ok";
+    case SD_EINVAL: return "invalid argument or configuration";
+    case SD_ENOMEM: return "KV block pool exhausted";
+    case SD_ESTATE: return "call not allowed in the slot's current state";
+    case SD_EHIP: return "HIP runtime error";
+    default: return "unknown error";
+  }
+}
+
+}  // extern "C"

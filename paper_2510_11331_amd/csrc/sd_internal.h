@@ -1,0 +1,179 @@
+// Internal declarations shared by the libsd kernels and host runtime.
+// Written for gfx950 (CDNA4): 64-lane wavefronts, bf16 MFMA, 160 KB LDS/CU.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sd {
+
+// ---------------------------------------------------------------- numerics
+
+typedef uint16_t bf16_t;  // raw bf16 bit pattern in memory
+
+__device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// round to nearest even (inputs are finite)
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+template <typename T> struct Store;
+template <> struct Store<bf16_t> {
+  __device__ __forceinline__ static float load(const bf16_t* p, size_t i) { return bf2f(p[i]); }
+  __device__ __forceinline__ static void store(bf16_t* p, size_t i, float v) { p[i] = f2bf(v); }
+};
+template <> struct Store<float> {
+  __device__ __forceinline__ static float load(const float* p, size_t i) { return p[i]; }
+  __device__ __forceinline__ static void store(float* p, size_t i, float v) { p[i] = v; }
+};
+
+// ---------------------------------------------------------------- row modes
+
+enum RowMode { ROWS_PREFILL = 0, ROWS_VERIFY = 1, ROWS_DRAFT_FIRST = 2, ROWS_DRAFT_NEXT = 3 };
+
+// per-slot device state, int32 x 4
+enum { ST_LEN = 0, ST_X0 = 1, ST_PEND = 2, ST_CAP = 3, ST_N = 4 };
+
+enum { ERR_KV_OVERFLOW = 1, ERR_BAD_TOKEN = 2, ERR_BAD_ACCEPT = 4 };
+
+// ---------------------------------------------------------------- kernel params
+
+struct RowsParams {
+  int mode, B, gamma, step_i, M;
+  const int32_t* slots;      // [B] (not prefill)
+  const int32_t* draft_tok;  // [B, gamma]
+  int32_t* state;            // [slots, ST_N]
+  int32_t* row_tok;          // [M]
+  int32_t* row_pos;          // [M]; -1 = inactive row
+  int32_t* row_slot;         // [M]
+  const void* embed;         // [V, d]
+  const void* gain;          // [d]
+  float* x;                  // [M, d]
+  void* xn;                  // [M, d]
+  int d, V, n_slots;
+  float eps;
+  int32_t* err;
+};
+
+struct NormParams {
+  const float* x;   // [rows_in, d]
+  const void* gain; // [d]
+  void* xn;         // [M, d]
+  int M, d, src_stride, src_off;  // output row r reads input row r*src_stride + src_off
+  float eps;
+};
+
+struct GemmParams {
+  const void* A;      // [M, K] activations
+  const void* W;      // [N, K] weights
+  int M, N, K;
+  int splits, chunks_per_split;
+  float* partial;     // [splits, M, N] when splits > 1
+  int* counters;      // [gridDim.x] zero between launches
+  float* out;         // STORE: out[m * ldo + n]; RESID: out[m * ldo + n] += acc
+  int ldo;
+  void* out_t;        // SWIGLU: out_t[m * (N/2) + f]
+};
+
+struct RopeParams {
+  const float* qkv;   // [M, (H + 2KV) hd]
+  float* q;           // [M, H hd]
+  void* kv;           // layer base of the pool: [blocks, 2, KV, 16, hd]
+  const int32_t* row_pos;
+  const int32_t* row_slot;
+  const int32_t* block_table;  // [slots, mbps]
+  const int32_t* state;
+  int M, H, KV, hd, mbps;
+  double theta;
+  int32_t* err;
+};
+
+struct AttnParams {
+  const float* q;            // [M, H hd] (rotary applied)
+  const void* kv;            // layer base of the pool
+  const int32_t* block_table;
+  int mbps;
+  const int32_t* row_pos;
+  const int32_t* row_slot;
+  const int32_t* rowblocks;  // [nrb, 2] = (row0, nrows), or null: rowblock i = rows [i*R, i*R+R)
+  int R, nrb, H, KV, hd;
+  int keys_per_split, splits;
+  float scale;
+  void* out;                 // [M, H hd] model dtype
+  float* part_o;             // [nrb*KV, splits, Qmax, hd]
+  float* part_ml;            // [nrb*KV, splits, Qmax, 2]
+  int* counters;             // [nrb*KV]
+  int qmax;                  // max query vectors per (rowblock, kv head)
+};
+
+struct SoftmaxParams {
+  const float* z;   // [M, V]
+  float* p;         // [M, V] (may alias z)
+  int M, V;
+  float inv_tau;
+  int greedy;
+};
+
+struct DraftSampleParams {
+  const float* z;          // [B, V] draft logits
+  float* q;                // [B, gamma, V]
+  int32_t* draft_tok;      // [B, gamma]
+  const uint32_t* u;       // [B, 2 gamma + 1]
+  int B, V, gamma, i;
+  float inv_tau;
+  int greedy;
+};
+
+struct AcceptParams {
+  int B, gamma, V, greedy;
+  const int32_t* draft_tok;  // [B, gamma]
+  const float* q;            // [B, gamma, V]
+  const float* p;            // [B, gamma+1, V]
+  const uint32_t* u;         // [B, 2 gamma + 1]
+  int32_t* n_acc;            // [B]
+  int32_t* out_tok;          // [B, gamma+1]
+  int32_t* err;              // may be null
+};
+
+struct CommitParams {
+  int B, gamma, n_slots;
+  const int32_t* slots;
+  const int32_t* n_acc;
+  const int32_t* out_tok;
+  int32_t* state;
+  int32_t* err;
+};
+
+enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+// ---------------------------------------------------------------- launchers
+// dtype: 0 bf16, 1 fp32 (same values as SD_DTYPE_*)
+
+hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s);
+hipError_t launch_rmsnorm(int dtype, const NormParams& p, hipStream_t s);
+hipError_t launch_gemm(int dtype, int epi, int mt, int grid_x, int grid_z,
+                       const GemmParams& p, hipStream_t s);
+hipError_t launch_rope_append(int dtype, const RopeParams& p, hipStream_t s);
+hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s);
+hipError_t launch_softmax(const SoftmaxParams& p, hipStream_t s);
+hipError_t launch_draft_sample(const DraftSampleParams& p, hipStream_t s);
+hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
+hipError_t launch_commit(const CommitParams& p, hipStream_t s);
+hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t s);
+
+// GEMM geometry (shared by host planning and the kernel)
+constexpr int GEMM_WAVES = 4;          // waves per workgroup, each a 16*NT column tile
+constexpr int GEMM_CHUNK = 256;        // bytes of a weight row streamed per step
+constexpr int GEMM_MROWS = 64;         // rows per M block (4 MFMA row tiles)
+inline int gemm_nt(int epi) { return epi == EPI_SWIGLU ? 2 : 1; }
+inline int gemm_cols_per_wg(int epi) { return GEMM_WAVES * 16 * gemm_nt(epi); }
+
+// attention geometry
+constexpr int ATTN_KEYS = 64;          // keys per LDS chunk
+constexpr int ATTN_QMAX = 64;          // max query vectors per workgroup
+
+}  // namespace sd
