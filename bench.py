@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Benchmark of the speculative-decoding hot path on one MI355X.
+
+Workload: LLaMA-7B-shaped bf16 target (32 layers, d 4096, 32 heads, FFN
+11008, vocab 32000) with a 2-layer d-1024 draft, B = 8 tasks, gamma = 4,
+prompts of 1024 uniform-random tokens, temperature 1.0, random-init weights.
+A step is one full pass of the hot path for the batch: gamma draft forwards
+with sampling, the verify forward over B*(gamma+1) rows, acceptance /
+resampling, and the KV commit.
+
+Prints one JSON line: verified tokens/s (emitted tokens of the timed steps /
+wall time), verify-step latency (HIP events, p50/p90), the roofline of the
+dominant kernel (the target's FFN gate/up GEMM), and the oracle timed on the
+host cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "verified tokens/sec + verify-step latency, 7B-shape bf16 B=8 gamma=4; HBM GB/s"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="7b_b8", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's batch size")
+    ap.add_argument("--gamma", type=int, default=0, help="override the workload's gamma")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def traffic_from_profiles(kernel_key: str):
+    """HBM bytes per launch of the dominant kernel, from the committed
+    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, copy-kernel scaled),
+    or None when no summary for the current kernel is committed."""
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+    try:
+        d = json.load(open(path))
+        e = d.get(kernel_key)
+        return None if e is None else float(e["bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def cpu_baseline(wl, B, gamma, emitted_per_step):
+    """The oracle (float64 NumPy, as it stands) on the host cores, on a
+    bounded sample of the workload: the verify pass (forward_rows over
+    gamma+1 rows with 1024 cached positions, LM head included) of every task
+    through a 1-layer and a 2-layer cut of the target, which separates the
+    per-layer cost from the head cost, and gamma draft forwards per task on
+    the full draft.  Scaled to a full step: head + n_layers * layer + drafts."""
+    from threadpoolctl import threadpool_info
+    from oracle import model as om
+    t, d = wl.target, wl.draft
+    ctx = wl.prompt_len
+    two = t.replace(n_layers=2)
+    w = synth.model_weights(two, 1)
+    m2 = om.Model(two, w)
+    m1 = om.Model.__new__(om.Model)                   # same float64 weights, first layer only
+    m1.s, m1.w, m1.bf16 = t.replace(n_layers=1), m2.w, m2.bf16
+    md = om.Model(d, synth.model_weights(d, 2))
+    rng = np.random.default_rng(0)
+
+    def cache(m, seed):
+        r = np.random.default_rng(seed)
+        c = m.new_cache()
+        for l in range(m.s.n_layers):
+            c.K[l] = m.r(r.standard_normal((ctx, m.s.n_kv_heads, m.s.head_dim)))
+            c.V[l] = m.r(r.standard_normal((ctx, m.s.n_kv_heads, m.s.head_dim)))
+        return c
+
+    def timed_verify(m):
+        tot = 0.0
+        for b in range(B):
+            c = cache(m, b)
+            rows = rng.integers(0, t.vocab, gamma + 1)
+            t0 = time.perf_counter()
+            m.forward_rows(c, rows)
+            tot += time.perf_counter() - t0
+        return tot
+
+    # repeat the sample until about 10 s of oracle time has been measured
+    reps, t1, t2, td, spent = 0, 0.0, 0.0, 0.0, 0.0
+    while reps == 0 or (spent < 10.0 and reps < 8):
+        a, b2 = timed_verify(m1), timed_verify(m2)
+        dd = 0.0
+        for b in range(B):
+            c = cache(md, 100 + b)
+            for i in range(gamma):
+                t0 = time.perf_counter()
+                md.decode_row(c, int(rng.integers(0, d.vocab)), len(c))
+                dd += time.perf_counter() - t0
+        t1, t2, td, reps = t1 + a, t2 + b2, td + dd, reps + 1
+        spent += a + b2 + dd
+    t1, t2, td = t1 / reps, t2 / reps, td / reps
+    layer = max(t2 - t1, 0.0)
+    head = max(t1 - layer, 0.0)
+    t_step = head + t.n_layers * layer + td
+    cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": emitted_per_step * B / t_step, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"float64 NumPy oracle, {B} tasks: verify of {gamma + 1} rows with {ctx} cached "
+                       f"positions through 1- and 2-layer cuts of the {t.n_layers}-layer target (LM head "
+                       f"included) and {gamma} draft forwards per task; scaled to a full step = "
+                       f"{t_step:.2f} s ({spent:.1f} s sampled over {reps} repetitions)"),
+            "step_seconds": round(t_step, 4)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
+              "the single-GPU figure is the per-GPU share of the task-sharded design.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2510_11331_amd import SDEngine, StepGraph, generate, generate_graph
+    from paper_2510_11331_amd import _lib
+
+    wl = synth.WORKLOADS[args.workload]
+    B = args.batch or wl.batch
+    gamma = args.gamma or wl.gamma
+    K, W = args.steps, args.warmup
+    t, d = wl.target, wl.draft
+    ctx_need = wl.prompt_len + (2 * K + W + 2) * (gamma + 1) + gamma + 16
+    print(f"[bench] workload {wl.name} B={B} gamma={gamma} steps={K} warmup={W}", file=sys.stderr, flush=True)
+
+    t0 = time.time()
+    tg, dg = synth.StreamingWeights(t, 1), synth.StreamingWeights(d, 2)
+    eng = SDEngine(t, d, tg, dg, max_slots=B, max_batch=B, gamma_max=gamma, max_ctx=ctx_need,
+                   prefill_rows=2048, temperature=wl.temperature, greedy=wl.greedy)
+    tg.close(); dg.close()
+    print(f"[bench] weights on device in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    prompts = synth.prompts(B, wl.prompt_len, t.vocab)
+    t0 = time.time()
+    eng.prefill(list(range(B)), prompts, [(2 * K + W + 2) * (gamma + 1)] * B)
+    print(f"[bench] prefill {B}x{wl.prompt_len} in {time.time() - t0:.2f}s", file=sys.stderr, flush=True)
+
+    batch = eng.batch(list(range(B)), gamma)
+    ut = synth.uniform_table(42, list(range(B)), W + 2 * K, gamma)
+    graph = StepGraph(eng, batch)                  # one HIP graph replays every step
+    generate_graph(eng, batch, ut[:W], W, graph)   # warmup
+    torch.cuda.synchronize()
+    # timed region: K graph replays, no host synchronisation inside
+    t0 = time.perf_counter()
+    acc, out = generate_graph(eng, batch, ut[W:W + K], K, graph)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    emitted = int((acc + 1).sum())
+    value = emitted / elapsed
+    print(f"[bench] timed {K} steps in {elapsed:.3f}s, {emitted} tokens", file=sys.stderr, flush=True)
+
+    # instrumented pass: HIP events on the launch stream around each kernel
+    # class.  Each step is queued behind a GPU sleep longer than its host
+    # enqueue time, so the events time kernels, not host launch latency.
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record(); torch.cuda._sleep(1_000_000); s1.record(); torch.cuda.synchronize()
+    cycles_per_ms = 1_000_000 / max(s0.elapsed_time(s1), 1e-3)
+    eng.profile(True)
+    verify_ms = []
+    for n in range(K):
+        torch.cuda._sleep(int(cycles_per_ms * 40))
+        generate(eng, [batch], [ut[W + K + n:W + K + n + 1]], 1, two_streams=False)
+        c, ms, _ = eng.profile_read(_lib.SD_PROF_VERIFY)
+        verify_ms.append(ms / max(c, 1))
+    n_gu, ms_gu, bytes_gu = eng.profile_read(_lib.SD_PROF_GEMM_VERIFY_GATEUP)
+    n_all, ms_all, bytes_all = eng.profile_read(_lib.SD_PROF_GEMM_VERIFY_ALL)
+    n_at, ms_at, _ = eng.profile_read(_lib.SD_PROF_ATTN_VERIFY)
+    n_dr, ms_dr, _ = eng.profile_read(_lib.SD_PROF_DRAFT)
+    eng.profile(False)
+    flags = eng.check_flags()
+    verify_ms = np.array(verify_ms)
+    gu_ms = ms_gu / max(n_gu, 1)
+    gu_bytes = bytes_gu / max(n_gu, 1)
+    achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
+    # algorithmic bytes of one verify step: every weight once, the cached K/V
+    # of every task once per layer, the new K/V, logits / probabilities
+    P = wl.prompt_len + (acc + 1).sum(0).mean() / 2
+    kv_bytes = t.n_layers * 2 * t.n_kv_heads * t.head_dim * 2 * B * P
+    step_bytes = 2 * t.n_params() + kv_bytes + 2 * B * (gamma + 1) * t.vocab * 4
+    verify_p50 = float(np.median(verify_ms))
+
+    res = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(elapsed / K * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: random-init N(0,0.02^2) bf16 weights, uniform-random prompt ids, SplitMix64 uniforms",
+        "config": {"workload": f"7B-shape target + 2-layer d1024 draft, B={B}, gamma={gamma}, "
+                               f"prompt {wl.prompt_len}, tau={wl.temperature}",
+                   "batch": B, "gamma": gamma, "prompt_len": wl.prompt_len, "temperature": wl.temperature},
+        "verify_ms_p50": round(verify_p50, 3),
+        "verify_ms_p90": round(float(np.percentile(verify_ms, 90)), 3),
+        "verify_hbm_gbs": round(step_bytes / (verify_p50 * 1e-3) / 1e9, 1),
+        "verify_hbm_frac": round(step_bytes / (verify_p50 * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "verify_gemm_gbs": round(bytes_all / max(ms_all, 1e-9) * 1e-6, 1),
+        "verify_attn_ms_per_layer": round(ms_at / max(n_at, 1), 4),
+        "draft_ms_per_call": round(ms_dr / max(n_dr, 1), 4),
+        "mean_accepted": round(float(acc.mean()), 4),
+        "mean_emitted_per_step": round(float((acc + 1).mean()), 4),
+        "device_flags": flags,
+        "roofline": {"kernel": "gemm_kernel<bf16, MT=3, NT=2, SWIGLU> (target FFN gate/up, M=40, N=22016, K=4096)",
+                     "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic_from_profiles("gemm_gateup_7b_b8"),
+                     "launch_ms": round(gu_ms, 5), "algorithmic_bytes_per_launch": gu_bytes},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        cb = cpu_baseline(wl, B, gamma, float((acc + 1).mean()))
+        res["cpu_baseline"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in cb.items()}
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

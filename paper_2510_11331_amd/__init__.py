@@ -5,4 +5,5 @@ work; this package holds its ctypes binding and a host driver that provides
 device memory and streams through PyTorch.
 """
 from ._lib import SDError, lib  # noqa: F401
-from .engine import SDEngine, Batch, GPUModel, generate, emitted_tokens, accept_resample  # noqa: F401
+from .engine import (SDEngine, Batch, GPUModel, StepGraph, generate, generate_graph,  # noqa: F401
+                     emitted_tokens, accept_resample)

@@ -24,7 +24,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 HIPCC_FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
+    "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++20",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
     "-I", INCLUDE, "-I", CSRC,

@@ -2,24 +2,37 @@
 // paged KV cache (Section II-A: eq. d_kv grows the cache by concatenation;
 // eq. d_atte / f21 attend with softmax(q K^T / sqrt(d0)) V).
 //
-// Paged layout of one layer's pool: [block][K|V][kv_head][16 tokens][hd] in
-// the model dtype; a slot's block table maps position / 16 to a block.
+// Paged layout of one layer's pool, per 16-token block and kv head: K as
+// [16 tokens][hd], V transposed as [hd][16 tokens] (so the P*V operand of a
+// matrix instruction is 4 consecutive tokens of one dimension); a slot's
+// block table maps position / 16 to a block.
 //
 // Attention work item = (row block, kv head, key split).  A row block is a
 // run of consecutive rows of one task (the gamma+1 verify rows of a task, its
-// 1-2 draft rows, or up to 64/G prefill rows); all G query heads of the kv
-// head and all rows of the block share every K/V tile, which is staged in
-// LDS 64 keys at a time.  Query i only sees keys at positions <= its own.
-// Each work item keeps an online softmax (running max, running sum,
-// rescaled output); when the keys are split, partial (max, sum, output)
-// triples go to a workspace and the last-arriving workgroup of the
-// (row block, kv head) merges them in split order.
+// 1-2 draft rows, or a run of prefill rows); all G query heads of the kv
+// head and all rows of the block are one set of query vectors that shares
+// every K/V tile.  Query i only sees keys at positions <= its own.  Each work
+// item keeps an online softmax (running max, running sum, rescaled output);
+// when the keys are split, partial (max, sum, output) triples go to a
+// workspace and the last-arriving workgroup of the (row block, kv head)
+// merges them in split order.
+//
+// bf16 models: S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_16x16x32_bf16,
+// 16 query vectors per wave, keys streamed from the cache straight into
+// registers 32 at a time (two blocks), one step ahead; q and p enter the
+// matrix instruction as bf16 hi + lo pairs, which keeps them at ~2^-16
+// relative precision.  fp32 models: a vector kernel with K/V staged in LDS.
 #include "sd_internal.h"
 
 namespace sd {
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 template <typename T>
 __global__ __launch_bounds__(256) void rope_append_kernel(RopeParams p) {
+  __shared__ float cs[64], sn[64];
   const int r = blockIdx.x;
   const int pos = p.row_pos[r];
   if (pos < 0) return;
@@ -32,16 +45,22 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeParams p) {
   const int off = pos % 16;
   T* kv = (T*)p.kv;
   const size_t kbase = (((size_t)blk * 2 + 0) * p.KV) * 16 * hd + (size_t)off * hd;
-  const size_t vbase = (((size_t)blk * 2 + 1) * p.KV) * 16 * hd + (size_t)off * hd;
+  const size_t vbase = (((size_t)blk * 2 + 1) * p.KV) * 16 * hd + off;
 
-  // thread -> frequency index i (fixed), heads strided; angle in float64
-  const int nh = p.H + p.KV;
-  for (int idx = threadIdx.x; idx < nh * half; idx += blockDim.x) {
-    const int i = idx % half, h = idx / half;
+  // angle pos * theta^(-2i/hd) in float64, once per frequency
+  if (threadIdx.x < half) {
+    const int i = threadIdx.x;
     const double ang = (double)pos * pow(p.theta, -2.0 * (double)i / (double)hd);
     double sd_, cd_;
     sincos(ang, &sd_, &cd_);
-    const float c = (float)cd_, s = (float)sd_;
+    cs[i] = (float)cd_;
+    sn[i] = (float)sd_;
+  }
+  __syncthreads();
+  const int nh = p.H + p.KV;
+  for (int idx = threadIdx.x; idx < nh * half; idx += blockDim.x) {
+    const int i = idx % half, h = idx / half;
+    const float c = cs[i], s = sn[i];
     if (h < p.H) {
       const float a = src[h * hd + i], b = src[h * hd + i + half];
       float* q = p.q + (size_t)r * Nq + h * hd;
@@ -57,7 +76,7 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeParams p) {
   if (ok) {
     for (int idx = threadIdx.x; idx < Nk; idx += blockDim.x) {
       const int kh = idx / hd, d = idx % hd;
-      Store<T>::store(kv, vbase + (size_t)kh * 16 * hd + d, src[Nq + Nk + idx]);
+      Store<T>::store(kv, vbase + (size_t)kh * 16 * hd + (size_t)d * 16, src[Nq + Nk + idx]);
     }
   } else if (threadIdx.x == 0) {
     atomicOr(p.err, ERR_KV_OVERFLOW);
@@ -164,17 +183,22 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
     for (int idx = tid; idx < 64 * UPR; idx += 256) {
       const int j = idx / UPR, e = (idx % UPR) * EPU;
       const int kp = c + j;
-      uint4 kk = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+      uint4 kk = make_uint4(0, 0, 0, 0);
+      T vv[EPU];
+#pragma unroll
+      for (int t = 0; t < EPU; ++t) vv[t] = T(0);
       if (kp < k_end) {
         const int blk = bt[kp / 16];
         const size_t base = (((size_t)blk * 2) * p.KV + kvh) * 16 * HD + (size_t)(kp % 16) * HD + e;
-        const size_t vbase = base + (size_t)p.KV * 16 * HD;
+        const size_t vtb = (((size_t)blk * 2 + 1) * p.KV + kvh) * 16 * HD + (kp % 16);
         kk = *(const uint4*)(kv + base);
-        vv = *(const uint4*)(kv + vbase);
+#pragma unroll
+        for (int t = 0; t < EPU; ++t) vv[t] = kv[vtb + (size_t)(e + t) * 16];   // V stored [hd][16]
       }
       uint32_t* kd = (uint32_t*)(Ks + j * KST + e);   // KST*esz is a multiple of 4
       kd[0] = kk.x; kd[1] = kk.y; kd[2] = kk.z; kd[3] = kk.w;
-      *(uint4*)(Vs + j * HD + e) = vv;
+#pragma unroll
+      for (int t = 0; t < EPU; ++t) Vs[j * HD + e + t] = vv[t];
     }
     __syncthreads();
     // scores and online softmax: wave w takes query vectors w, w+4, ...; lane = key
@@ -269,8 +293,275 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
   if (tid == 0) p.counters[rbk] = 0;
 }
 
+// bf16 hi + lo pair of 8 floats, packed as two bf16x8 operands
+__device__ __forceinline__ void split8(const float (&x)[8], u32x4& hi, u32x4& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const bf16_t a0 = f2bf(x[2 * k]), a1 = f2bf(x[2 * k + 1]);
+    const bf16_t b0 = f2bf(x[2 * k] - bf2f(a0)), b1 = f2bf(x[2 * k + 1] - bf2f(a1));
+    h[k] = (uint32_t)a0 | ((uint32_t)a1 << 16);
+    l[k] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+  }
+  hi = u32x4{h[0], h[1], h[2], h[3]};
+  lo = u32x4{l[0], l[1], l[2], l[3]};
+}
+
+__device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                 c, 0, 0, 0);
+}
+
+// Wave w of a workgroup (8 waves) takes query tile w % QTe (16 query
+// vectors) and key group w / QTe: 32-key steps kb = k_begin + 32 (kg + KG j).
+// Lane (r16, g): query r16 of the tile; in S^T it holds keys 4g..4g+3 of
+// both blocks of the step, in O^T dimensions 16 dt + 4g .. +3.
+constexpr int ATTN_WAVES = 8;
+
+template <int HD>
+__global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnParams p) {
+  constexpr int UPG = HD / 32;             // 16-byte K units per lane group (HD/4 dims)
+  constexpr int DT = HD / 16;              // 16-dimension output tiles
+  __shared__ float s_o[4][16][HD + 4];        // one slot per query tile
+  __shared__ float s_m[4][16], s_l[4][16];
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int rbk = blockIdx.x;
+  const int rb = rbk / p.KV, kvh = rbk % p.KV;
+  const int split = blockIdx.y;
+  int row0, nr;
+  if (p.rowblocks) {
+    row0 = p.rowblocks[2 * rb];
+    nr = p.rowblocks[2 * rb + 1];
+  } else {
+    row0 = rb * p.R;
+    nr = p.R;
+  }
+  const int G = p.H / p.KV;
+  const int Qn = nr * G;
+  const int QT = (Qn + 15) >> 4;
+  const int QTe = QT == 3 ? 4 : QT;
+  const int KG = ATTN_WAVES / QTe;
+  const int qt = wave % QTe, kg = wave / QTe;
+  const bool wave_on = qt < QT;
+
+  int maxpos = -1;
+  for (int r = 0; r < nr; ++r) maxpos = max(maxpos, p.row_pos[row0 + r]);
+  const int slot = p.row_slot[row0];
+  const int k_begin = split * p.keys_per_split;
+  const int k_end = min(min(k_begin + p.keys_per_split, maxpos + 1), p.mbps * 16);
+
+  const int qi = qt * 16 + r16;
+  const bool qvalid = wave_on && qi < Qn;
+  const int qrow = row0 + (qvalid ? qi / G : 0);
+  const int qh = kvh * G + (qvalid ? qi % G : 0);
+  const int qpos = qvalid ? p.row_pos[qrow] : -1;
+
+  u32x4 qhi[UPG], qlo[UPG];
+  {
+    const float* qs = p.q + (size_t)qrow * p.H * HD + (size_t)qh * HD + g * (HD / 4);
+#pragma unroll
+    for (int s = 0; s < UPG; ++s) {
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = qvalid ? qs[8 * s + e] * p.scale : 0.f;
+      split8(x, qhi[s], qlo[s]);
+    }
+  }
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[DT];
+#pragma unroll
+  for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const bf16_t* kv = (const bf16_t*)p.kv;
+  const int32_t* bt = p.block_table + (size_t)slot * p.mbps;
+  const size_t blk_stride = (size_t)2 * p.KV * 16 * HD;
+  const size_t koff = (size_t)kvh * 16 * HD + (size_t)r16 * HD + g * (HD / 4);
+  const size_t voff = (size_t)p.KV * 16 * HD + (size_t)kvh * 16 * HD + (size_t)r16 * 16 + 4 * g;
+
+  // two register stages of one 32-key step: K rows (two blocks) and V^T quads
+  u32x4 Kf[2][2][UPG];
+  uint32_t Vf[2][2][DT][2];
+
+  auto load = [&]<int S>(int kb) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int bi = kb / 16 + t;
+      const bool ok = bi < p.mbps && kb + 16 * t < k_end;
+      const bf16_t* base = kv + (size_t)(ok ? bt[bi] : 0) * blk_stride;
+#pragma unroll
+      for (int s = 0; s < UPG; ++s) Kf[S][t][s] = *(const u32x4*)(base + koff + 8 * s);
+      // keys at or past k_end were never written: their scores are masked, and
+      // their V entries are zeroed so that p = 0 never meets a NaN/Inf pattern
+      const int nq = min(max(k_end - (kb + 16 * t + 4 * g), 0), 4);
+      const uint32_t mx = nq >= 2 ? 0xffffffffu : (nq == 1 ? 0xffffu : 0u);
+      const uint32_t my = nq >= 4 ? 0xffffffffu : (nq == 3 ? 0xffffu : 0u);
+#pragma unroll
+      for (int d = 0; d < DT; ++d) {
+        const uint2 v = *(const uint2*)(base + voff + (size_t)d * 256);
+        Vf[S][t][d][0] = v.x & mx;
+        Vf[S][t][d][1] = v.y & my;
+      }
+    }
+  };
+  auto step = [&]<int S>(int kb) {
+    f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+    for (int s = 0; s < UPG; ++s) {
+      s0 = mfma_bf16(Kf[S][0][s], qhi[s], s0);
+      s0 = mfma_bf16(Kf[S][0][s], qlo[s], s0);
+      s1 = mfma_bf16(Kf[S][1][s], qhi[s], s1);
+      s1 = mfma_bf16(Kf[S][1][s], qlo[s], s1);
+    }
+    float sc[8];
+    bool ok[8];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int k0 = kb + 4 * g + v, k1 = k0 + 16;
+      ok[v] = k0 < k_end && k0 <= qpos;
+      ok[4 + v] = k1 < k_end && k1 <= qpos;
+      sc[v] = s0[v];
+      sc[4 + v] = s1[v];
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) mx = ok[e] ? fmaxf(mx, sc[e]) : mx;
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m_run, mx);
+    float pe[8], sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      pe[e] = ok[e] ? expf(sc[e] - mnew) : 0.f;
+      sum += pe[e];
+    }
+    sum += __shfl_xor(sum, 16);
+    sum += __shfl_xor(sum, 32);
+    const float alpha = m_run == -INFINITY ? 0.f : expf(m_run - mnew);
+    l_run = l_run * alpha + sum;
+    m_run = mnew;
+    u32x4 phi, plo;
+    split8(pe, phi, plo);
+#pragma unroll
+    for (int d = 0; d < DT; ++d) {
+      o[d] *= alpha;
+      const u32x4 va = u32x4{Vf[S][0][d][0], Vf[S][0][d][1], Vf[S][1][d][0], Vf[S][1][d][1]};
+      o[d] = mfma_bf16(va, phi, o[d]);
+      o[d] = mfma_bf16(va, plo, o[d]);
+    }
+  };
+
+  const int kstep = 32 * KG;
+  int kb = k_begin + 32 * kg;
+  if (wave_on && kb < k_end) {
+    load.template operator()<0>(kb);
+    for (; kb < k_end; kb += 2 * kstep) {
+      const int kb1 = kb + kstep;
+      if (kb1 < k_end) load.template operator()<1>(kb1);
+      step.template operator()<0>(kb);
+      if (kb1 >= k_end) break;
+      const int kb2 = kb1 + kstep;
+      if (kb2 < k_end) load.template operator()<0>(kb2);
+      step.template operator()<1>(kb1);
+    }
+  }
+
+  // merge the key groups of a query tile into key group 0, in key-group
+  // order: in round k, key group k hands its state over through the slot of
+  // its query tile
+  for (int k = 1; k < KG; ++k) {
+    if (wave_on && kg == k) {
+      if (g == 0) {
+        s_m[qt][r16] = m_run;
+        s_l[qt][r16] = l_run;
+      }
+#pragma unroll
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s_o[qt][r16][16 * d + 4 * g + v] = o[d][v];
+    }
+    __syncthreads();
+    if (wave_on && kg == 0) {
+      const float mb = s_m[qt][r16], lb = s_l[qt][r16];
+      const float M = fmaxf(m_run, mb);
+      const float a = m_run == -INFINITY ? 0.f : expf(m_run - M);
+      const float b = mb == -INFINITY ? 0.f : expf(mb - M);
+      l_run = l_run * a + lb * b;
+#pragma unroll
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) o[d][v] = o[d][v] * a + s_o[qt][r16][16 * d + 4 * g + v] * b;
+      m_run = M;
+    }
+    __syncthreads();
+  }
+  const bool owner = wave_on && kg == 0 && qvalid;
+  bf16_t* out = (bf16_t*)p.out + (size_t)qrow * p.H * HD + (size_t)qh * HD;
+
+  if (p.splits == 1) {
+    if (owner) {
+      const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+#pragma unroll
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) out[16 * d + 4 * g + v] = f2bf(o[d][v] * inv);
+    }
+    return;
+  }
+
+  const size_t item = ((size_t)rbk * p.splits + split) * p.qmax + (owner ? qi : 0);
+  if (owner) {
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) p.part_o[item * HD + 16 * d + 4 * g + v] = o[d][v];
+    if (g == 0) {
+      p.part_ml[item * 2] = m_run;
+      p.part_ml[item * 2 + 1] = l_run;
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) s_last = atomicAdd(&p.counters[rbk], 1) == p.splits - 1;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  if (owner) {
+    const size_t base = (size_t)rbk * p.splits * p.qmax + qi;
+    float M = -INFINITY;
+    for (int sp = 0; sp < p.splits; ++sp) M = fmaxf(M, p.part_ml[(base + (size_t)sp * p.qmax) * 2]);
+    float L = 0.f;
+    f32x4 O[DT];
+#pragma unroll
+    for (int d = 0; d < DT; ++d) O[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (M != -INFINITY) {
+      for (int sp = 0; sp < p.splits; ++sp) {
+        const size_t it = base + (size_t)sp * p.qmax;
+        const float m = p.part_ml[it * 2];
+        if (m == -INFINITY) continue;
+        const float w = expf(m - M);
+        L += p.part_ml[it * 2 + 1] * w;
+#pragma unroll
+        for (int d = 0; d < DT; ++d)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) O[d][v] += p.part_o[it * HD + 16 * d + 4 * g + v] * w;
+      }
+    }
+    const float inv = L > 0.f ? 1.0f / L : 0.f;
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) out[16 * d + 4 * g + v] = f2bf(O[d][v] * inv);
+  }
+  if (tid == 0) p.counters[rbk] = 0;
+}
+
 hipError_t launch_rope_append(int dtype, const RopeParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
+  if (p.hd > 128) return hipErrorInvalidValue;
   if (dtype == 0) hipLaunchKernelGGL(rope_append_kernel<bf16_t>, dim3(p.M), dim3(256), 0, s, p);
   else hipLaunchKernelGGL(rope_append_kernel<float>, dim3(p.M), dim3(256), 0, s, p);
   return hipGetLastError();
@@ -293,13 +584,16 @@ static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s) {
 hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s) {
   if (p.nrb <= 0) return hipSuccess;
   if (p.qmax > ATTN_QMAX) return hipErrorInvalidValue;
+  if (p.keys_per_split % 64) return hipErrorInvalidValue;
+  const dim3 grid(p.nrb * p.KV, p.splits);
   if (dtype == 0) {
-    if (p.hd == 64) return launch_attn_t<bf16_t, 64>(p, s);
-    if (p.hd == 128) return launch_attn_t<bf16_t, 128>(p, s);
-  } else {
-    if (p.hd == 64) return launch_attn_t<float, 64>(p, s);
-    if (p.hd == 128) return launch_attn_t<float, 128>(p, s);
+    if (p.hd == 64) hipLaunchKernelGGL(attention_mfma_kernel<64>, grid, dim3(64 * ATTN_WAVES), 0, s, p);
+    else if (p.hd == 128) hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(64 * ATTN_WAVES), 0, s, p);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
   }
+  if (p.hd == 64) return launch_attn_t<float, 64>(p, s);
+  if (p.hd == 128) return launch_attn_t<float, 128>(p, s);
   return hipErrorInvalidValue;
 }
 

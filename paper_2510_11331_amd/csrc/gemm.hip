@@ -4,22 +4,24 @@
 //
 // The pass is bound by streaming W from HBM, so the kernel is organised
 // around that stream:
-//   * each wave owns NT 16-row tiles of W (16*NT output columns) and streams
-//     them straight from global memory into registers, 256 contiguous bytes
-//     of a row per step and lane group (no LDS round trip: every weight byte
-//     is used by exactly one wave), one step ahead of the MFMAs;
-//   * the activations A[M, K-range] are shared by the 4 waves of a workgroup
-//     and staged through LDS in 256-byte column chunks, double buffered;
-//   * the K permutation inside a chunk is the same for A and W, so each lane
-//     reads 64 contiguous bytes of its weight row per step;
+//   * a workgroup owns one column tile (16*NT output columns = 16*NT rows
+//     of W; NT in {1, 2, 4, 8}, wider tiles re-read the activations less
+//     often) and splits K over its KW waves (up to 16); each wave streams its
+//     K slice of the tile's W rows straight into registers, 64-128
+//     contiguous bytes of a row per step, one step ahead of the MFMAs;
+//   * the matching activation fragments A[rows, K slice] are loaded the same
+//     way (they are small and stay in L2), so the main loop has no LDS
+//     traffic and no barriers, and vmcnt only ever waits for the older step;
+//   * the K permutation inside a step is the same for A and W, so a lane
+//     reads 16-32 contiguous bytes of its weight row per step;
 //   * bf16: one v_mfma_f32_16x16x32_bf16 per 16-byte unit; fp32: four
 //     v_mfma_f32_16x16x4_f32;
-//   * K is split over gridDim.y when the column tiles alone cannot fill the
-//     256 CUs; partial tiles go to a workspace and the last-arriving
-//     workgroup of a column tile adds them in split order (deterministic)
-//     and runs the epilogue.
-// Epilogues: store fp32, add into the fp32 residual stream, or SwiGLU over
-// interleaved gate/up rows (written in the model dtype).
+//   * the KW partial tiles are added in wave order through LDS
+//     (deterministic); K is never split across workgroups (a cross-workgroup
+//     reduction needs a device-scope release per workgroup, which costs more
+//     than it recovers at these sizes);
+//   * epilogues: store fp32, add into the fp32 residual stream, or SwiGLU
+//     over interleaved gate/up rows (written in the model dtype).
 #include "sd_internal.h"
 
 namespace sd {
@@ -47,31 +49,45 @@ template <> struct Mfma<float> {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
 
-template <typename T, int MT, int NT, int EPI>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
-  constexpr int ROWB = GEMM_CHUNK + 16;          // LDS row stride (bytes), padded
-  constexpr int UNITS = GEMM_CHUNK / 64;         // 16-byte units per lane group per step
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][MT * 16 * ROWB];
-  __shared__ int s_last;
+template <int MT, int NT> struct GemmBounds {
+  static constexpr int threads = (MT >= 3 || NT >= 4) ? 512 : 1024;
+};
+
+// Lane (r16, g) streams bytes [16 U g, 16 U (g + 1)) of each 64 U-byte step
+// of its weight rows; the activation fragments use the same bytes, so the K
+// permutation inside a step is shared by both operands.  Waves walk their K
+// slice starting at a workgroup-dependent rotation, which spreads the
+// concurrent activation reads of different workgroups over the L2 channels.
+template <typename T, int MT, int NT, int U, int EPI>
+__global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(GemmParams p) {
+  constexpr int CB = 64 * U;               // bytes of a row per step
+  __shared__ float red[4][MT * NT * 4][64];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int KW = blockDim.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const size_t kbytes = (size_t)p.K * sizeof(T);
+  const int total = (int)(kbytes / CB);
+  const int c0 = 0, c1 = total;
+  const int per = (c1 - c0 + KW - 1) / KW;
+  const int wc0 = min(c0 + wave * per, c1), wc1 = min(wc0 + per, c1);
+  const int nw = wc1 - wc0;
+  const int rot = nw > 0 ? (int)((blockIdx.x * 7u) % (unsigned)nw) : 0;
+  const int n0 = blockIdx.x * 16 * NT;
   const int m0 = blockIdx.z * MT * 16;
-  const int split = blockIdx.y;
-  const int n_wave = (blockIdx.x * GEMM_WAVES + wave) * 16 * NT;
-  const bool active = n_wave < p.N;
-  const int total_chunks = (int)(kbytes / GEMM_CHUNK);
-  const int c0 = split * p.chunks_per_split;
-  const int c1 = min(c0 + p.chunks_per_split, total_chunks);
 
-  const unsigned char* A = (const unsigned char*)p.A;
   const unsigned char* wrow[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j)
-    wrow[j] = (const unsigned char*)p.W + (size_t)(active ? n_wave + 16 * j + r16 : 0) * kbytes + g * 64;
-
-  const int arow = tid >> 4, acol = (tid & 15) * 16;
+    wrow[j] = (const unsigned char*)p.W + (size_t)(n0 + 16 * j + r16) * kbytes + g * 16 * U;
+  const unsigned char* arow[MT];
+  bool aval[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int m = m0 + 16 * i + r16;
+    aval[i] = m < p.M;
+    arow[i] = (const unsigned char*)p.A + (size_t)(aval[i] ? m : 0) * kbytes + g * 16 * U;
+  }
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -79,104 +95,70 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 w0[NT][UNITS], w1[NT][UNITS], ab[MT];
-
-  auto load_w = [&](u32x4 (&w)[NT][UNITS], int c) {
+  u32x4 ws[2][NT][U], as[2][MT][U];
+  auto load = [&]<int S>(int i) {              // i-th step of this wave's slice
+    int c = wc0 + i + rot;
+    if (c >= wc1) c -= nw;
+    const size_t off = (size_t)c * CB;
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int u = 0; u < UNITS; ++u)
-        w[j][u] = *(const u32x4*)(wrow[j] + (size_t)c * GEMM_CHUNK + u * 16);
+      for (int u = 0; u < U; ++u) ws[S][j][u] = *(const u32x4*)(wrow[j] + off + u * 16);
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        as[S][t][u] = aval[t] ? *(const u32x4*)(arow[t] + off + u * 16) : u32x4{0u, 0u, 0u, 0u};
   };
-  auto load_a = [&](int c) {
+  auto compute = [&]<int S>() {
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const int m = m0 + arow + 16 * i;
-      ab[i] = m < p.M ? *(const u32x4*)(A + (size_t)m * kbytes + (size_t)c * GEMM_CHUNK + acol)
-                      : u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-  auto store_a = [&](unsigned char* L) {
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-    for (int i = 0; i < MT; ++i) *(u32x4*)(L + (arow + 16 * i) * ROWB + acol) = ab[i];
-  };
-  auto compute = [&](const unsigned char* L, u32x4 (&w)[NT][UNITS]) {
+      for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int u = 0; u < UNITS; ++u) {
-#pragma unroll
-      for (int i = 0; i < MT; ++i) {
-        const u32x4 af = *(const u32x4*)(L + (i * 16 + r16) * ROWB + g * 64 + u * 16);
-#pragma unroll
-        for (int j = 0; j < NT; ++j) acc[i][j] = Mfma<T>::step(af, w[j][u], acc[i][j]);
-      }
-    }
+        for (int j = 0; j < NT; ++j) acc[t][j] = Mfma<T>::step(as[S][t][u], ws[S][j][u], acc[t][j]);
   };
 
-  if (c0 < c1) {
-    if (active) load_w(w0, c0);
-    load_a(c0);
-    store_a(lds[0]);
-    __syncthreads();
-    for (int c = c0; c < c1; c += 2) {
-      const bool has1 = c + 1 < c1;
-      if (has1) {
-        if (active) load_w(w1, c + 1);
-        load_a(c + 1);
-      }
-      if (active) compute(lds[0], w0);
-      if (has1) store_a(lds[1]);
-      __syncthreads();
-      if (!has1) break;
-      const bool has2 = c + 2 < c1;
-      if (has2) {
-        if (active) load_w(w0, c + 2);
-        load_a(c + 2);
-      }
-      if (active) compute(lds[1], w1);
-      if (has2) store_a(lds[0]);
-      __syncthreads();
+  if (nw > 0) {
+    load.template operator()<0>(0);
+    for (int i = 0; i < nw; i += 2) {
+      if (i + 1 < nw) load.template operator()<1>(i + 1);
+      compute.template operator()<0>();
+      if (i + 1 >= nw) break;
+      if (i + 2 < nw) load.template operator()<0>(i + 2);
+      compute.template operator()<1>();
     }
   }
 
-  // accumulator element (i, j, v) is row m0 + 16 i + 4 g + v, column n_wave + 16 j + r16
-  if (p.splits > 1) {
-    if (active) {
+  // wave partials -> wave 0, four waves per round, added in wave order
+  for (int base = 0; base < KW; base += 4) {
+    const int slot = wave - base;
+    if (wave != 0 && slot >= 0 && slot < 4) {
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
         for (int j = 0; j < NT; ++j)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int m = m0 + 16 * i + 4 * g + v;
-            if (m < p.M)
-              p.partial[((size_t)split * p.M + m) * p.N + n_wave + 16 * j + r16] = acc[i][j][v];
-          }
+          for (int v = 0; v < 4; ++v) red[slot][(i * NT + j) * 4 + v][lane] = acc[i][j][v];
     }
-    __threadfence();
     __syncthreads();
-    if (tid == 0) s_last = atomicAdd(&p.counters[blockIdx.x], 1) == p.splits - 1;
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    if (active) {
+    if (wave == 0) {
+      for (int s = 0; s < 4; ++s) {
+        const int w = base + s;
+        if (w == 0 || w >= KW) continue;
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+        for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int j = 0; j < NT; ++j)
+          for (int j = 0; j < NT; ++j)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int m = m0 + 16 * i + 4 * g + v;
-            float s = 0.f;
-            if (m < p.M)
-              for (int sp = 0; sp < p.splits; ++sp)
-                s += p.partial[((size_t)sp * p.M + m) * p.N + n_wave + 16 * j + r16];
-            acc[i][j][v] = s;
-          }
+            for (int v = 0; v < 4; ++v) acc[i][j][v] += red[s][(i * NT + j) * 4 + v][lane];
+      }
     }
-    if (tid == 0) p.counters[blockIdx.x] = 0;
+    __syncthreads();
   }
-  if (!active) return;
+  if (wave != 0) return;
 
+  // accumulator element (i, j, v) is row m0 + 16 i + 4 g + v, column n0 + 16 j + r16
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -184,14 +166,15 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
       const int m = m0 + 16 * i + 4 * g + v;
       if (m >= p.M) continue;
       if constexpr (EPI == EPI_SWIGLU) {
+        // tiles (2k, 2k+1) are the gate and up rows of the same 16 outputs
         const int F = p.N / 2;
-        const int f = n_wave / 2 + r16;
-        const float gate = acc[i][0][v], up = acc[i][1][v];
-        Store<T>::store((T*)p.out_t, (size_t)m * F + f, silu(gate) * up);
+#pragma unroll
+        for (int j = 0; j < NT; j += 2)
+          Store<T>::store((T*)p.out_t, (size_t)m * F + n0 / 2 + 8 * j + r16, silu(acc[i][j][v]) * acc[i][j + 1][v]);
       } else {
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
-          float* o = p.out + (size_t)m * p.ldo + n_wave + 16 * j + r16;
+          float* o = p.out + (size_t)m * p.ldo + n0 + 16 * j + r16;
           if constexpr (EPI == EPI_RESID) *o += acc[i][j][v];
           else *o = acc[i][j][v];
         }
@@ -199,30 +182,57 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     }
 }
 
-template <typename T, int EPI>
-static hipError_t launch_mt(int mt, dim3 grid, const GemmParams& p, hipStream_t s) {
-  constexpr int NT = EPI == EPI_SWIGLU ? 2 : 1;
+template <typename T, int EPI, int NT, int U>
+static hipError_t launch_mt(int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s) {
   switch (mt) {
-    case 1: hipLaunchKernelGGL((gemm_kernel<T, 1, NT, EPI>), grid, dim3(256), 0, s, p); break;
-    case 2: hipLaunchKernelGGL((gemm_kernel<T, 2, NT, EPI>), grid, dim3(256), 0, s, p); break;
-    case 3: hipLaunchKernelGGL((gemm_kernel<T, 3, NT, EPI>), grid, dim3(256), 0, s, p); break;
-    case 4: hipLaunchKernelGGL((gemm_kernel<T, 4, NT, EPI>), grid, dim3(256), 0, s, p); break;
+    case 1: hipLaunchKernelGGL((gemm_kernel<T, 1, NT, U, EPI>), grid, dim3(threads), 0, s, p); break;
+    case 2: hipLaunchKernelGGL((gemm_kernel<T, 2, NT, U, EPI>), grid, dim3(threads), 0, s, p); break;
+    case 3:
+      if constexpr (NT <= 4) {
+        hipLaunchKernelGGL((gemm_kernel<T, 3, NT, U, EPI>), grid, dim3(threads), 0, s, p);
+        break;
+      }
+      return hipErrorInvalidValue;
+    case 4:
+      // 64-row blocks (prefill) only with tiles of up to 32 columns
+      if constexpr (NT <= 2) {
+        hipLaunchKernelGGL((gemm_kernel<T, 4, NT, U, EPI>), grid, dim3(threads), 0, s, p);
+        break;
+      }
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(int dtype, int epi, int mt, int grid_x, int grid_z, const GemmParams& p,
-                       hipStream_t s) {
-  dim3 grid(grid_x, p.splits, grid_z);
-  if (dtype == 0) {
-    if (epi == EPI_STORE) return launch_mt<bf16_t, EPI_STORE>(mt, grid, p, s);
-    if (epi == EPI_RESID) return launch_mt<bf16_t, EPI_RESID>(mt, grid, p, s);
-    return launch_mt<bf16_t, EPI_SWIGLU>(mt, grid, p, s);
+template <typename T, int EPI>
+static hipError_t launch_nt(int nt, int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s) {
+  switch (nt) {
+    case 1:
+      if constexpr (EPI != EPI_SWIGLU) return launch_mt<T, EPI, 1, 2>(mt, grid, threads, p, s);
+      return hipErrorInvalidValue;
+    case 2: return launch_mt<T, EPI, 2, 2>(mt, grid, threads, p, s);
+    case 4: return launch_mt<T, EPI, 4, 2>(mt, grid, threads, p, s);
+    case 8: return launch_mt<T, EPI, 8, 1>(mt, grid, threads, p, s);
+    default: return hipErrorInvalidValue;
   }
-  if (epi == EPI_STORE) return launch_mt<float, EPI_STORE>(mt, grid, p, s);
-  if (epi == EPI_RESID) return launch_mt<float, EPI_RESID>(mt, grid, p, s);
-  return launch_mt<float, EPI_SWIGLU>(mt, grid, p, s);
+}
+
+int gemm_step_bytes(int nt) { return nt == 8 ? 64 : 128; }
+
+hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int grid_z, const GemmParams& p,
+                       hipStream_t s) {
+  if (kw < 1 || kw > ((mt >= 3 || nt >= 4) ? 8 : 16)) return hipErrorInvalidValue;
+  dim3 grid(grid_x, 1, grid_z);
+  const int threads = 64 * kw;
+  if (dtype == 0) {
+    if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, p, s);
+    if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, p, s);
+    return launch_nt<bf16_t, EPI_SWIGLU>(nt, mt, grid, threads, p, s);
+  }
+  if (epi == EPI_STORE) return launch_nt<float, EPI_STORE>(nt, mt, grid, threads, p, s);
+  if (epi == EPI_RESID) return launch_nt<float, EPI_RESID>(nt, mt, grid, threads, p, s);
+  return launch_nt<float, EPI_SWIGLU>(nt, mt, grid, threads, p, s);
 }
 
 }  // namespace sd

@@ -14,6 +14,8 @@
 
 namespace sd {
 
+constexpr int RV = 8;   // float4 per thread: rows of up to 8192 entries stay in registers
+
 __device__ __forceinline__ float block_sum256(float v, float* red) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -24,14 +26,43 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
+template <typename T> struct Vec4;
+template <> struct Vec4<bf16_t> {
+  __device__ __forceinline__ static float4 load(const bf16_t* p, int i4) {
+    const uint2 u = ((const uint2*)p)[i4];
+    return make_float4(bf2f((bf16_t)(u.x & 0xffff)), bf2f((bf16_t)(u.x >> 16)), bf2f((bf16_t)(u.y & 0xffff)),
+                       bf2f((bf16_t)(u.y >> 16)));
+  }
+  __device__ __forceinline__ static void store(bf16_t* p, int i4, float4 v) {
+    ((uint2*)p)[i4] = make_uint2((uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16),
+                                 (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+  }
+};
+template <> struct Vec4<float> {
+  __device__ __forceinline__ static float4 load(const float* p, int i4) { return ((const float4*)p)[i4]; }
+  __device__ __forceinline__ static void store(float* p, int i4, float4 v) { ((float4*)p)[i4] = v; }
+};
+
+// out = x / sqrt(mean(x^2) + eps) * gain for a register-resident row
+// (float4 i of the row is v[k] with i = threadIdx.x + 256 k)
 template <typename T>
-__device__ void norm_row(const float* x, const T* gain, T* out, int d, float eps, float* red) {
+__device__ void norm_store(const float4 (&v)[RV], int d, const T* gain, T* out, float eps, float* red) {
+  const int d4 = d >> 2;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) ss += x[i] * x[i];
+#pragma unroll
+  for (int k = 0; k < RV; ++k)
+    if (threadIdx.x + 256 * k < d4) ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
   ss = block_sum256(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256)
-    Store<T>::store(out, i, x[i] * inv * Store<T>::load(gain, i));
+#pragma unroll
+  for (int k = 0; k < RV; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    if (i < d4) {
+      const float4 g = Vec4<T>::load(gain, i);
+      Vec4<T>::store(out, i, make_float4(v[k].x * inv * g.x, v[k].y * inv * g.y, v[k].z * inv * g.z,
+                                         v[k].w * inv * g.w));
+    }
+  }
 }
 
 template <typename T>
@@ -89,23 +120,42 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
     if (threadIdx.x == 0) atomicOr(p.err, ERR_BAD_TOKEN);
     tok = 0;
   }
-  float* x = p.x + (size_t)r * p.d;
+  const int d4 = p.d >> 2;
   const T* e = (const T*)p.embed + (size_t)tok * p.d;
-  for (int i = threadIdx.x; i < p.d; i += 256) x[i] = pos >= 0 ? Store<T>::load(e, i) : 0.f;
-  __syncthreads();
-  norm_row<T>(x, (const T*)p.gain, (T*)p.xn + (size_t)r * p.d, p.d, p.eps, red);
+  float4* x = (float4*)(p.x + (size_t)r * p.d);
+  float4 v[RV];
+#pragma unroll
+  for (int k = 0; k < RV; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i < d4 && pos >= 0) v[k] = Vec4<T>::load(e, i);
+  }
+#pragma unroll
+  for (int k = 0; k < RV; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    if (i < d4) x[i] = v[k];
+  }
+  norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn + (size_t)r * p.d, p.eps, red);
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(NormParams p) {
   __shared__ float red[4];
   const int r = blockIdx.x;
-  const float* x = p.x + ((size_t)r * p.src_stride + p.src_off) * p.d;
-  norm_row<T>(x, (const T*)p.gain, (T*)p.xn + (size_t)r * p.d, p.d, p.eps, red);
+  const float4* x = (const float4*)(p.x + ((size_t)r * p.src_stride + p.src_off) * p.d);
+  const int d4 = p.d >> 2;
+  float4 v[RV];
+#pragma unroll
+  for (int k = 0; k < RV; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    v[k] = i < d4 ? x[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn + (size_t)r * p.d, p.eps, red);
 }
 
 hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
+  if ((p.d & 3) || p.d > 256 * 4 * RV) return hipErrorInvalidValue;
   if (dtype == 0) hipLaunchKernelGGL(rows_embed_kernel<bf16_t>, dim3(p.M), dim3(256), 0, s, p);
   else hipLaunchKernelGGL(rows_embed_kernel<float>, dim3(p.M), dim3(256), 0, s, p);
   return hipGetLastError();
@@ -113,6 +163,7 @@ hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s) {
 
 hipError_t launch_rmsnorm(int dtype, const NormParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
+  if ((p.d & 3) || p.d > 256 * 4 * RV) return hipErrorInvalidValue;
   if (dtype == 0) hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(p.M), dim3(256), 0, s, p);
   else hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(p.M), dim3(256), 0, s, p);
   return hipGetLastError();

@@ -13,51 +13,92 @@
 //            T = floor(S r / 2^32) from 32-bit halves, smallest j with
 //            prefix_j > T;
 //   residual w_j = max(0, p_j - q_j) with a correctly rounded float32 subtract.
+//
+// A row (up to 32768 entries) is held in registers by one 1024-thread
+// workgroup: for sampling each thread owns 32 consecutive entries (so the
+// prefix sum in index order is one block scan of per-thread totals); the
+// plain softmax uses a strided float4 layout for coalescing.  All loads of a
+// row are issued before any is used.
 #include "sd_internal.h"
 
 namespace sd {
 
-constexpr int RB = 256;   // threads per row kernel
+constexpr int RT = 1024;          // threads of a row kernel
+constexpr int NW = RT / 64;       // waves
+constexpr int SEG = 32;           // consecutive entries per thread in sampling kernels
+constexpr int SV = SEG / 4;       // float4 per thread in the strided layout (V <= RT * 4 * SV)
 
-__device__ __forceinline__ float bmax(float v, float* red) {
+__device__ __forceinline__ float wmax(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  return v;
 }
-__device__ __forceinline__ float bsum(float v, float* red) {
+__device__ __forceinline__ float wsum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ float block_max(float v, float* red) {
+  v = wmax(v);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
-  return red[0] + red[1] + red[2] + red[3];
+  float r = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) r = fmaxf(r, red[w]);
+  return r;
+}
+__device__ float block_sum(float v, float* red) {
+  v = wsum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) r += red[w];
+  return r;
 }
 
-// arg-max over a row, lowest index on ties
-__device__ int bargmax(const float* z, int V, float* redv, int* redi) {
-  float bv = -INFINITY;
-  int bi = 0x7fffffff;
-  for (int j = threadIdx.x; j < V; j += RB) {
-    const float v = z[j];
-    if (v > bv) { bv = v; bi = j; }       // strided ascending: first hit is the lowest index
-  }
+// arg-max with the lowest index on ties
+__device__ int block_argmax(float v, int i, float* redv, int* redi) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(bv, o);
-    const int oi = __shfl_xor(bi, o);
-    if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+    const float ov = __shfl_xor(v, o);
+    const int oi = __shfl_xor(i, o);
+    if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
   }
   __syncthreads();
-  if ((threadIdx.x & 63) == 0) { redv[threadIdx.x >> 6] = bv; redi[threadIdx.x >> 6] = bi; }
+  if ((threadIdx.x & 63) == 0) { redv[threadIdx.x >> 6] = v; redi[threadIdx.x >> 6] = i; }
   __syncthreads();
-  float v = redv[0];
-  int i = redi[0];
-  for (int w = 1; w < 4; ++w)
-    if (redv[w] > v || (redv[w] == v && redi[w] < i)) { v = redv[w]; i = redi[w]; }
-  return i == 0x7fffffff ? 0 : i;
+  float bv = redv[0];
+  int bi = redi[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w)
+    if (redv[w] > bv || (redv[w] == bv && redi[w] < bi)) { bv = redv[w]; bi = redi[w]; }
+  return bi;
+}
+
+// exclusive prefix of per-thread uint64 values in thread order; *total = sum
+__device__ uint64_t block_excl_scan(uint64_t v, uint64_t* red, uint64_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned long long x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  __syncthreads();
+  if (lane == 63) red[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t a = 0;
+    for (int w = 0; w < NW; ++w) { const uint64_t t = red[w]; red[w] = a; a += t; }
+    red[NW] = a;
+  }
+  __syncthreads();
+  *total = red[NW];
+  return red[wave] + x - v;
 }
 
 __device__ __forceinline__ uint64_t fixed40(float w) {
@@ -65,91 +106,155 @@ __device__ __forceinline__ uint64_t fixed40(float w) {
   return w > 0.f ? (uint64_t)(w * 1099511627776.0f) : 0ull;
 }
 
-// Integer inverse-CDF draw with weights wf(j), j < V; returns -1 if S == 0.
-// Thread t owns the contiguous index range [t*seg, (t+1)*seg).
-template <typename WF>
-__device__ int block_sample(WF wf, int V, uint32_t r, uint64_t* part, int* result) {
-  const int seg = (V + RB - 1) / RB;
-  const int j0 = min(V, (int)threadIdx.x * seg), j1 = min(V, j0 + seg);
-  uint64_t local = 0;
-  for (int j = j0; j < j1; ++j) local += fixed40(wf(j));
-  __syncthreads();
-  part[threadIdx.x] = local;
-  if (threadIdx.x == 0) *result = -1;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint64_t acc = 0;
-    for (int t = 0; t < RB; ++t) { const uint64_t v = part[t]; part[t] = acc; acc += v; }
-    part[RB] = acc;
+// thread-contiguous segment of a row: entries [SEG*t, SEG*t + SEG) (0 beyond V)
+__device__ __forceinline__ void load_seg(const float* row, int V, float (&v)[SEG]) {
+  const int j0 = threadIdx.x * SEG;
+  if (j0 + SEG <= V && (V & 3) == 0) {
+#pragma unroll
+    for (int k = 0; k < SV; ++k) {
+      const float4 x = *(const float4*)(row + j0 + 4 * k);
+      v[4 * k] = x.x; v[4 * k + 1] = x.y; v[4 * k + 2] = x.z; v[4 * k + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < SEG; ++k) v[k] = j0 + k < V ? row[j0 + k] : 0.f;
   }
-  __syncthreads();
-  const uint64_t S = part[RB];
+}
+
+// Integer inverse-CDF draw over the weights w (this thread's segment);
+// returns -1 if S == 0.
+__device__ int seg_sample(const float (&w)[SEG], uint32_t r, uint64_t* red, int* result) {
+  uint64_t local = 0;
+#pragma unroll
+  for (int k = 0; k < SEG; ++k) local += fixed40(w[k]);
+  if (threadIdx.x == 0) *result = -1;
+  uint64_t S;
+  const uint64_t lo = block_excl_scan(local, red, &S);
   if (S == 0) return -1;
   const uint64_t T = (S >> 32) * (uint64_t)r + (((S & 0xffffffffull) * (uint64_t)r) >> 32);
-  const uint64_t lo = part[threadIdx.x];
-  if (T >= lo && T < lo + local) {
-    uint64_t acc = lo;
-    for (int j = j0; j < j1; ++j) {
-      acc += fixed40(wf(j));
-      if (acc > T) { *result = j; break; }
+  if (T >= lo && T < lo + local) {                // this thread's segment holds the draw
+    int hit = SEG - 1;
+    uint64_t pre = lo;
+#pragma unroll
+    for (int k = 0; k < SEG; ++k) {                // smallest k with lo + prefix_k > T
+      pre += fixed40(w[k]);
+      if (pre > T) { hit = k; break; }
     }
+    *result = threadIdx.x * SEG + hit;
   }
   __syncthreads();
   return *result;
 }
 
-// softmax(z / tau) of one row into out (may alias z)
-__device__ void row_softmax(const float* z, float* out, int V, float inv_tau, float* red) {
-  float m = -INFINITY;
-  for (int j = threadIdx.x; j < V; j += RB) m = fmaxf(m, z[j] * inv_tau);
-  m = bmax(m, red);
-  float s = 0.f;
-  for (int j = threadIdx.x; j < V; j += RB) s += expf(z[j] * inv_tau - m);
-  s = bsum(s, red);
-  __syncthreads();
-  for (int j = threadIdx.x; j < V; j += RB) out[j] = expf(z[j] * inv_tau - m) / s;
-  __syncthreads();
-}
-
-__global__ __launch_bounds__(RB) void softmax_kernel(SoftmaxParams p) {
-  __shared__ float red[4];
+__global__ __launch_bounds__(RT) void softmax_kernel(SoftmaxParams p) {
+  __shared__ float red[NW];
   const float* z = p.z + (size_t)blockIdx.x * p.V;
   float* out = p.p + (size_t)blockIdx.x * p.V;
+  const int V4 = p.V >> 2;
+  float4 x[SV];
+#pragma unroll
+  for (int k = 0; k < SV; ++k) {
+    const int i = threadIdx.x + RT * k;
+    x[k] = i < V4 ? ((const float4*)z)[i] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+  }
   if (p.greedy) {
     if (out != z)
-      for (int j = threadIdx.x; j < p.V; j += RB) out[j] = z[j];
+#pragma unroll
+      for (int k = 0; k < SV; ++k) {
+        const int i = threadIdx.x + RT * k;
+        if (i < V4) ((float4*)out)[i] = x[k];
+      }
     return;
   }
-  row_softmax(z, out, p.V, p.inv_tau, red);
+  float m = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < SV; ++k) {
+    x[k].x *= p.inv_tau; x[k].y *= p.inv_tau; x[k].z *= p.inv_tau; x[k].w *= p.inv_tau;
+    m = fmaxf(m, fmaxf(fmaxf(x[k].x, x[k].y), fmaxf(x[k].z, x[k].w)));
+  }
+  m = block_max(m, red);
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < SV; ++k) {
+    x[k].x = expf(x[k].x - m); x[k].y = expf(x[k].y - m); x[k].z = expf(x[k].z - m); x[k].w = expf(x[k].w - m);
+    s += (x[k].x + x[k].y) + (x[k].z + x[k].w);
+  }
+  s = block_sum(s, red);
+#pragma unroll
+  for (int k = 0; k < SV; ++k) {
+    const int i = threadIdx.x + RT * k;
+    if (i < V4) ((float4*)out)[i] = make_float4(x[k].x / s, x[k].y / s, x[k].z / s, x[k].w / s);
+  }
 }
 
-__global__ __launch_bounds__(RB) void draft_sample_kernel(DraftSampleParams p) {
-  __shared__ float red[4];
-  __shared__ float redv[4];
-  __shared__ int redi[4];
-  __shared__ uint64_t part[RB + 1];
+__global__ __launch_bounds__(RT) void draft_sample_kernel(DraftSampleParams p) {
+  __shared__ float red[NW];
+  __shared__ int redi[NW];
+  __shared__ uint64_t redu[NW + 1];
   __shared__ int result;
   const int b = blockIdx.x;
   const float* z = p.z + (size_t)b * p.V;
   float* q = p.q + ((size_t)b * p.gamma + p.i) * p.V;
+  const int j0 = threadIdx.x * SEG;
+  float v[SEG];
+  load_seg(z, p.V, v);
   int tok;
   if (p.greedy) {
-    for (int j = threadIdx.x; j < p.V; j += RB) q[j] = z[j];
-    tok = bargmax(z, p.V, redv, redi);
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int k = 0; k < SEG; ++k)
+      if (j0 + k < p.V && v[k] > bv) { bv = v[k]; bi = j0 + k; }
+    tok = block_argmax(bv, bi, red, redi);
+    if (tok == 0x7fffffff) tok = 0;
+#pragma unroll
+    for (int k = 0; k < SEG; ++k)
+      if (j0 + k < p.V) q[j0 + k] = v[k];
   } else {
-    row_softmax(z, q, p.V, p.inv_tau, red);
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < SEG; ++k) {
+      v[k] *= p.inv_tau;
+      if (j0 + k < p.V) m = fmaxf(m, v[k]);
+    }
+    m = block_max(m, red);
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < SEG; ++k) {
+      v[k] = j0 + k < p.V ? expf(v[k] - m) : 0.f;
+      s += v[k];
+    }
+    s = block_sum(s, red);
+#pragma unroll
+    for (int k = 0; k < SEG; ++k) {
+      v[k] = v[k] / s;
+      if (j0 + k < p.V) q[j0 + k] = v[k];
+    }
     const uint32_t r = p.u[(size_t)b * (2 * p.gamma + 1) + p.i];
-    tok = block_sample([&](int j) { return q[j]; }, p.V, r, part, &result);
-    if (tok < 0) tok = bargmax(z, p.V, redv, redi);    // no integer mass: cannot happen for a softmax row
+    tok = seg_sample(v, r, redu, &result);
+    if (tok < 0) tok = 0;                       // no integer mass: impossible for a softmax row
   }
   if (threadIdx.x == 0) p.draft_tok[b * p.gamma + p.i] = tok;
 }
 
-__global__ __launch_bounds__(RB) void accept_kernel(AcceptParams p) {
-  __shared__ float redv[4];
-  __shared__ int redi[4];
-  __shared__ uint64_t part[RB + 1];
-  __shared__ int result, s_a, s_y;
+__device__ int row_argmax(const float* row, int V, float* red, int* redi) {
+  float v[SEG];
+  load_seg(row, V, v);
+  const int j0 = threadIdx.x * SEG;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+#pragma unroll
+  for (int k = 0; k < SEG; ++k)
+    if (j0 + k < V && v[k] > bv) { bv = v[k]; bi = j0 + k; }
+  const int r = block_argmax(bv, bi, red, redi);
+  return r == 0x7fffffff ? 0 : r;
+}
+
+__global__ __launch_bounds__(RT) void accept_kernel(AcceptParams p) {
+  __shared__ float red[NW];
+  __shared__ int redi[NW];
+  __shared__ uint64_t redu[NW + 1];
+  __shared__ int result, s_a;
   const int b = blockIdx.x, g = p.gamma, V = p.V;
   const int32_t* dt = p.draft_tok + (size_t)b * g;
   const float* q = p.q + (size_t)b * g * V;
@@ -158,10 +263,10 @@ __global__ __launch_bounds__(RB) void accept_kernel(AcceptParams p) {
   int a = g, y = 0;
   if (p.greedy) {
     for (int i = 0; i < g; ++i) {
-      const int am = bargmax(pp + (size_t)i * V, V, redv, redi);
+      const int am = row_argmax(pp + (size_t)i * V, V, red, redi);
       if (dt[i] != am) { a = i; y = am; break; }
     }
-    if (a == g) y = bargmax(pp + (size_t)g * V, V, redv, redi);
+    if (a == g) y = row_argmax(pp + (size_t)g * V, V, red, redi);
   } else {
     if (threadIdx.x == 0) {
       int aa = g;
@@ -181,22 +286,25 @@ __global__ __launch_bounds__(RB) void accept_kernel(AcceptParams p) {
     __syncthreads();
     a = s_a;
     const uint32_t r = u[2 * g];
+    float w[SEG];
+    load_seg(pp + (size_t)a * V, V, w);
     if (a < g) {
-      const float* pa = pp + (size_t)a * V;
-      const float* qa = q + (size_t)a * V;
-      y = block_sample([&](int j) { const float d = __fsub_rn(pa[j], qa[j]); return d > 0.f ? d : 0.f; },
-                       V, r, part, &result);
-      if (y < 0) y = block_sample([&](int j) { return pa[j]; }, V, r, part, &result);
+      float res[SEG];
+      load_seg(q + (size_t)a * V, V, res);
+#pragma unroll
+      for (int k = 0; k < SEG; ++k) {
+        const float d = __fsub_rn(w[k], res[k]);
+        res[k] = d > 0.f ? d : 0.f;
+      }
+      y = seg_sample(res, r, redu, &result);
+      if (y < 0) y = seg_sample(w, r, redu, &result);      // residual without integer mass
     } else {
-      const float* pg = pp + (size_t)g * V;
-      y = block_sample([&](int j) { return pg[j]; }, V, r, part, &result);
+      y = seg_sample(w, r, redu, &result);
     }
     if (y < 0) y = 0;
   }
-  if (threadIdx.x == 0) { s_y = y; }
-  __syncthreads();
-  for (int i = threadIdx.x; i <= g; i += RB)
-    p.out_tok[(size_t)b * (g + 1) + i] = i < a ? dt[i] : (i == a ? s_y : -1);
+  for (int i = threadIdx.x; i <= g; i += RT)
+    p.out_tok[(size_t)b * (g + 1) + i] = i < a ? dt[i] : (i == a ? y : -1);
   if (threadIdx.x == 0) p.n_acc[b] = a;
 }
 
@@ -223,17 +331,20 @@ __global__ void commit_kernel(CommitParams p) {
 
 hipError_t launch_softmax(const SoftmaxParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(softmax_kernel, dim3(p.M), dim3(RB), 0, s, p);
+  if (p.V > RT * SEG || (p.V & 3)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(softmax_kernel, dim3(p.M), dim3(RT), 0, s, p);
   return hipGetLastError();
 }
 hipError_t launch_draft_sample(const DraftSampleParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(draft_sample_kernel, dim3(p.B), dim3(RB), 0, s, p);
+  if (p.V > RT * SEG) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(draft_sample_kernel, dim3(p.B), dim3(RT), 0, s, p);
   return hipGetLastError();
 }
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(RB), 0, s, p);
+  if (p.V > RT * SEG) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(RT), 0, s, p);
   return hipGetLastError();
 }
 hipError_t launch_commit(const CommitParams& p, hipStream_t s) {

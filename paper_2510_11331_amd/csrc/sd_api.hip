@@ -107,7 +107,7 @@ bool model_ok(const sd_model_cfg& m) {
   const size_t e = esize(m.dtype);
   // GEMM K dims stream in 256-byte chunks; N dims come in 16-column tiles
   if ((m.d_model * e) % GEMM_CHUNK || (m.d_ffn * e) % GEMM_CHUNK) return false;
-  if (m.vocab % 16 || m.d_ffn % 16) return false;
+  if (m.vocab % 16 || m.d_ffn % 16 || m.vocab > 32768) return false;   // row kernels hold <= 32768 entries
   if (!(m.rope_theta > 0.f) || !(m.rms_eps > 0.f)) return false;
   return true;
 }
@@ -191,7 +191,7 @@ void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int q
   const int nmax = std::max(std::max(D.nqkv, D.d), std::max(2 * D.F, D.V));
   ln.partial_cap = (size_t)MAX_SPLITS * std::min(rows, GEMM_MROWS) * nmax;
   ln.partial = al.take<float>(sizeof(float) * ln.partial_cap);
-  ln.gemm_cnt_n = (nmax + 63) / 64 + 1;
+  ln.gemm_cnt_n = nmax / 16 + 1;
   ln.gemm_cnt = al.take<int>(sizeof(int) * ln.gemm_cnt_n);
   ln.attn_cnt_n = decode_rb * D.KV;
   ln.attn_o_cap = (size_t)ln.attn_cnt_n * splits * qmax_dec * D.hd;
@@ -261,40 +261,50 @@ void prof_end(sd_ctx* ctx, hipStream_t s, ProfRec& r) {
 // ---------------------------------------------------------------- GEMM planning
 
 struct GemmPlan {
-  int mt, gx, gz, splits, cps;
+  int nt, mt, kw, gx, gz, splits, cps;
 };
 
+// One column tile of 16*nt columns per workgroup, kw waves splitting K inside
+// it.  Measured on MI355X at M = 40 (7B-shape verify): the widest tile that
+// still leaves ~170+ workgroups is fastest (wider tiles re-read the
+// activations less often), with 4 waves for 128-column tiles and 8 waves
+// otherwise.  K is not split across workgroups: the cross-workgroup
+// reduction needs a device-scope release per workgroup, which costs more
+// than it recovers at these sizes.
 GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, size_t partial_cap) {
+  (void)partial_cap;
   GemmPlan g{};
   g.gz = (M + GEMM_MROWS - 1) / GEMM_MROWS;
   g.mt = g.gz > 1 ? 4 : (M + 15) / 16;
-  g.gx = (N + gemm_cols_per_wg(epi) - 1) / gemm_cols_per_wg(epi);
-  const int chunks = (int)(K * esz / GEMM_CHUNK);
-  int splits = 1;
-  if (g.gz == 1) {
-    const int target_wgs = 512;
-    splits = std::min(std::min(MAX_SPLITS, chunks), std::max(1, (target_wgs + g.gx - 1) / g.gx));
-    while (splits > 1 && (size_t)splits * M * N > partial_cap) --splits;
+  g.nt = epi == EPI_SWIGLU ? 2 : 1;
+  for (int nt : {8, 4, 2}) {
+    // register file: 48-row tiles take at most 64 columns, 64-row blocks 32
+    if ((g.mt == 4 && nt > 2) || (g.mt == 3 && nt > 4)) continue;
+    if (nt > g.nt && N % (16 * nt) == 0 && N / (16 * nt) >= 170) {
+      g.nt = nt;
+      break;
+    }
   }
-  g.cps = (chunks + splits - 1) / splits;
-  g.splits = (chunks + g.cps - 1) / g.cps;
+  g.gx = N / (16 * g.nt);
+  const int steps = (int)(K * esz / gemm_step_bytes(g.nt));
+  const int kw_max = (g.mt >= 3 || g.nt >= 4) ? 8 : 16;
+  const int kw_pref = g.nt == 8 ? 4 : kw_max;
+  g.kw = std::max(1, std::min(kw_pref, steps / 2));
+  g.splits = 1;
+  g.cps = steps;
   return g;
 }
 
 int gemm(sd_ctx* ctx, Lane& ln, const ModelRT& m, int epi, const void* A, const void* W, int M, int N,
          int K, float* out, int ldo, void* out_t, hipStream_t s, int prof_kind, int prof_kind2) {
   const GemmPlan g = plan_gemm(M, N, K, m.esz, epi, ln.partial_cap);
-  if (g.gx + 1 > ln.gemm_cnt_n && g.splits > 1) return SD_EINVAL;
+  if (N % (16 * g.nt)) return SD_EINVAL;
   GemmParams p{};
   p.A = A;
   p.W = W;
   p.M = M;
   p.N = N;
   p.K = K;
-  p.splits = g.splits;
-  p.chunks_per_split = g.cps;
-  p.partial = ln.partial;
-  p.counters = ln.gemm_cnt;
   p.out = out;
   p.ldo = ldo;
   p.out_t = out_t;
@@ -304,7 +314,7 @@ int gemm(sd_ctx* ctx, Lane& ln, const ModelRT& m, int epi, const void* A, const 
   ProfRec r1, r2;
   prof_begin(ctx, s, r1, prof_kind, bytes);
   prof_begin(ctx, s, r2, prof_kind2, bytes);
-  HIPCHK(launch_gemm(m.c.dtype == SD_DTYPE_F32 ? 1 : 0, epi, g.mt, g.gx, g.gz, p, s));
+  HIPCHK(launch_gemm(m.c.dtype == SD_DTYPE_F32 ? 1 : 0, epi, g.nt, g.mt, g.kw, g.gx, g.gz, p, s));
   prof_end(ctx, s, r2);
   prof_end(ctx, s, r1);
   return SD_OK;
@@ -368,8 +378,17 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.H = c.n_heads;
     ap.KV = c.n_kv_heads;
     ap.hd = c.head_dim;
-    ap.splits = attn_splits;
-    ap.keys_per_split = attn_splits > 1 ? ctx->keys_per_split : ctx->cfg.max_ctx;
+    // split the keys only when the (row block, kv head) items alone leave the
+    // chip idle: a split costs a device-scope release per workgroup
+    int splits = attn_splits;
+    if (splits > 1) {
+      const int items = nrb * c.n_kv_heads;
+      splits = std::min(splits, std::max(1, (256 + items - 1) / items));
+    }
+    const int kps = (ctx->cfg.max_ctx + 63) / 64 * 64;
+    ap.splits = splits;
+    ap.keys_per_split = splits > 1 ? std::max(ctx->keys_per_split, (kps / splits + 63) / 64 * 64) : kps;
+    ap.splits = splits > 1 ? (kps + ap.keys_per_split - 1) / ap.keys_per_split : 1;
     ap.scale = 1.0f / sqrtf((float)c.head_dim);
     ap.out = ln.att;
     ap.part_o = ln.attn_o;
@@ -693,7 +712,8 @@ int sd_verify(sd_ctx* ctx, int B, const int32_t* slots, int gamma, const int32_t
 
 int sd_accept_resample(int B, int gamma, int vocab, int greedy, const int32_t* draft_tok, const float* q,
                        const float* p, const uint32_t* u, int32_t* n_acc, int32_t* out_tok, void* stream) {
-  if (B < 1 || gamma < 1 || gamma > 64 || vocab < 1 || !draft_tok || !q || !p || !u || !n_acc || !out_tok)
+  if (B < 1 || gamma < 1 || gamma > 64 || vocab < 1 || vocab > 32768 || !draft_tok || !q || !p || !u || !n_acc ||
+      !out_tok)
     return SD_EINVAL;
   AcceptParams ap{};
   ap.B = B;

@@ -71,9 +71,6 @@ struct GemmParams {
   const void* A;      // [M, K] activations
   const void* W;      // [N, K] weights
   int M, N, K;
-  int splits, chunks_per_split;
-  float* partial;     // [splits, M, N] when splits > 1
-  int* counters;      // [gridDim.x] zero between launches
   float* out;         // STORE: out[m * ldo + n]; RESID: out[m * ldo + n] += acc
   int ldo;
   void* out_t;        // SWIGLU: out_t[m * (N/2) + f]
@@ -155,7 +152,7 @@ enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 
 hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s);
 hipError_t launch_rmsnorm(int dtype, const NormParams& p, hipStream_t s);
-hipError_t launch_gemm(int dtype, int epi, int mt, int grid_x, int grid_z,
+hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int grid_z,
                        const GemmParams& p, hipStream_t s);
 hipError_t launch_rope_append(int dtype, const RopeParams& p, hipStream_t s);
 hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s);
@@ -166,11 +163,9 @@ hipError_t launch_commit(const CommitParams& p, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t s);
 
 // GEMM geometry (shared by host planning and the kernel)
-constexpr int GEMM_WAVES = 4;          // waves per workgroup, each a 16*NT column tile
-constexpr int GEMM_CHUNK = 256;        // bytes of a weight row streamed per step
+constexpr int GEMM_CHUNK = 128;        // K dims must be a multiple of this many bytes
 constexpr int GEMM_MROWS = 64;         // rows per M block (4 MFMA row tiles)
-inline int gemm_nt(int epi) { return epi == EPI_SWIGLU ? 2 : 1; }
-inline int gemm_cols_per_wg(int epi) { return GEMM_WAVES * 16 * gemm_nt(epi); }
+int gemm_step_bytes(int nt);           // bytes of a weight row per wave step for tile width nt
 
 // attention geometry
 constexpr int ATTN_KEYS = 64;          // keys per LDS chunk

@@ -209,6 +209,25 @@ class SDEngine:
         return int(n.value), float(ms.value), float(by.value)
 
 
+class StepGraph:
+    """One SD step of a batch (gamma draft calls, verify, accept, commit)
+    captured as a HIP graph.  Every launch reads per-step data from device
+    memory (slot state, uniforms), so one capture replays every step: before
+    each replay the step's uniforms are copied into the captured buffer.
+    Capturing records launches only; it does not advance any state."""
+
+    def __init__(self, engine: "SDEngine", b: Batch):
+        self.engine, self.b = engine, b
+        self.u = torch.zeros(b.B, 2 * b.gamma + 1, dtype=torch.int32, device=engine.device)
+        self.g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.g):
+            engine.step(b, self.u)
+
+    def run(self, u_step: torch.Tensor) -> None:
+        self.u.copy_(u_step)
+        self.g.replay()
+
+
 def accept_resample(B, gamma, vocab, greedy, draft_tok, q, p, u, n_acc, out_tok, stream=None) -> None:
     """Context-free acceptance / resampling kernel (sd_accept_resample)."""
     check(lib().sd_accept_resample(B, gamma, vocab, int(bool(greedy)), _ptr(draft_tok), _ptr(q), _ptr(p),
@@ -218,6 +237,23 @@ def accept_resample(B, gamma, vocab, greedy, draft_tok, q, p, u, n_acc, out_tok,
 def uniforms_device(table: np.ndarray, device="cuda") -> torch.Tensor:
     """uint32 uniforms -> a device int32 tensor with the same bits."""
     return torch.from_numpy(np.ascontiguousarray(table).view(np.int32)).to(device)
+
+
+def generate_graph(engine: SDEngine, batch: Batch, utable: np.ndarray, n_steps: int,
+                   graph: Optional[StepGraph] = None):
+    """n_steps SD steps of one batch by graph replay on the current stream;
+    returns (n_acc [n_steps, B], out_tok [n_steps, B, gamma+1]) on the host."""
+    dev = engine.device
+    u = uniforms_device(utable, dev)
+    graph = graph or StepGraph(engine, batch)
+    hist_acc = torch.empty(n_steps, batch.B, dtype=torch.int32, device=dev)
+    hist_out = torch.empty(n_steps, batch.B, batch.gamma + 1, dtype=torch.int32, device=dev)
+    for n in range(n_steps):
+        graph.run(u[n])
+        hist_acc[n].copy_(batch.n_acc)
+        hist_out[n].copy_(batch.out_tok)
+    torch.cuda.synchronize(dev)
+    return hist_acc.cpu().numpy(), hist_out.cpu().numpy()
 
 
 def generate(engine: SDEngine, batches: List[Batch], utables: List[np.ndarray], n_steps: int,

@@ -285,3 +285,35 @@ def uniform_table(seed: int, tasks: Sequence[int], n_steps: int, gamma: int) -> 
     """uint32 [n_steps, len(tasks), 2*gamma+1]."""
     n = 2 * gamma + 1
     return np.stack([uniforms(seed, tasks, st, n) for st in range(n_steps)])
+
+
+class StreamingWeights:
+    """Callable name -> array that generates a model's weights on a thread
+    pool, at most `window` tensors ahead of the consumer, in the order of
+    weight_names(shape).  Any order works; out-of-order names are generated
+    on demand."""
+
+    def __init__(self, shape: ModelShape, seed: int, workers: Optional[int] = None, window: int = 24):
+        self.shape, self.seed = shape, seed
+        self.shapes = weight_shapes(shape)
+        self.order = weight_names(shape)
+        self.window = window
+        self.ex = ThreadPoolExecutor(max_workers=workers or min(16, len(os.sched_getaffinity(0))))
+        self.fut: Dict[str, object] = {}
+        self.next = 0
+        self._fill()
+
+    def _fill(self):
+        while self.next < len(self.order) and len(self.fut) < self.window:
+            n = self.order[self.next]
+            self.fut[n] = self.ex.submit(gen_tensor, self.seed, n, self.shapes[n], self.shape.dtype)
+            self.next += 1
+
+    def __call__(self, name: str) -> np.ndarray:
+        f = self.fut.pop(name, None)
+        a = f.result() if f is not None else gen_tensor(self.seed, name, self.shapes[name], self.shape.dtype)
+        self._fill()
+        return a
+
+    def close(self):
+        self.ex.shutdown(wait=False, cancel_futures=True)

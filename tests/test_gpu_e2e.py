@@ -149,3 +149,47 @@ def test_small_bf16_gqa_logits_and_greedy():
         worst = max(worst, np.abs(z0 - zr).max() / np.abs(zr).max())
     assert worst < 2e-2
     print("bf16 row-0 rel logit error", worst)
+
+
+@pytest.mark.parametrize("kind", ["tiny", "bf16"])
+def test_graph_replay_equals_eager(kind):
+    """A captured step replayed many times, with eager work and host
+    synchronisation between replays, gives the eager result at every step."""
+    say("graph replay", kind)
+    import torch
+    from paper_2510_11331_amd import generate, StepGraph
+    from paper_2510_11331_amd.engine import uniforms_device
+    if kind == "tiny":
+        t, d, tw, dw = tiny_pair("perturbed")
+        tau = 0.2
+    else:
+        t = synth.ModelShape(2, 512, 8, 2, 1024, 2048, "bf16")
+        d = synth.ModelShape(1, 256, 4, 4, 512, 2048, "bf16")
+        tw, dw = synth.model_weights(t, 31), synth.model_weights(d, 32)
+        tau = 1.0
+    gamma, n_steps = 4, 6
+    prompts = synth.prompts(2, 30, t.vocab, first_task=3)
+    ut = synth.uniform_table(8, [0, 1], n_steps, gamma)
+    res = []
+    for use_graph in (False, True):
+        eng = make_engine(t, d, tw, dw, max_slots=2, max_batch=2, gamma_max=gamma,
+                          max_ctx=30 + (n_steps + 1) * (gamma + 1) + 8, temperature=tau)
+        eng.prefill([0, 1], prompts, [n_steps * (gamma + 1)] * 2)
+        b = eng.batch([0, 1], gamma)
+        if not use_graph:
+            [(acc, out)] = generate(eng, [b], [ut], n_steps, two_streams=False)
+        else:
+            g = StepGraph(eng, b)
+            u = uniforms_device(ut)
+            accs, outs = [], []
+            for n in range(n_steps):
+                g.run(u[n])
+                torch.cuda.synchronize()
+                accs.append(b.n_acc.cpu().numpy().copy())
+                outs.append(b.out_tok.cpu().numpy().copy())
+                _ = torch.ones(1000, device="cuda").sum()        # eager work between replays
+            acc, out = np.stack(accs), np.stack(outs)
+        assert eng.check_flags() == 0
+        res.append((acc, out))
+        eng.close()
+    assert np.array_equal(res[0][0], res[1][0]) and np.array_equal(res[0][1], res[1][1])
