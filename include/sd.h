@@ -34,7 +34,8 @@
  *   - A negative return value is an error (SD_E*).  Argument and state
  *     errors are detected on the host before anything is enqueued and leave
  *     the context unchanged.  No C++ exception crosses this interface.
- *   - Layouts are row-major.  bf16 data is stored as raw 16-bit patterns.
+ *   - Layouts are row-major except the packed weight matrices described at
+ *     sd_pack_linear.  bf16 data is stored as raw 16-bit patterns.
  *   - Calls that share one context and overlap in time on different streams
  *     must use disjoint slots, and at most one draft call and one
  *     verify/accept/commit sequence may be in flight at a time (they use
@@ -76,8 +77,10 @@ typedef struct {
 } sd_model_cfg;
 
 /* Weights of one model, in the model's dtype.  Matrices are [out, in]
- * (y = x W^T).  The per-layer pointer arrays are host arrays of n_layers
- * device pointers; sd_init copies them.
+ * (y = x W^T); wqkv, wo, wgu, wdown and lm_head must be given in the packed
+ * layout that sd_pack_linear writes (embed and the norms stay row-major).
+ * The per-layer pointer arrays are host arrays of n_layers device pointers;
+ * sd_init copies them.
  *   wqkv  [(n_heads + 2 n_kv_heads) head_dim, d_model]: query rows (head
  *         major), then key rows, then value rows.
  *   wo    [d_model, n_heads head_dim]
@@ -109,6 +112,19 @@ typedef struct {
     void *workspace;        /* sd_workspace_bytes(cfg) bytes                */
     size_t workspace_bytes;
 } sd_config;
+
+/* Repack a row-major [N, K] matrix of dtype (SD_DTYPE_*) into the layout
+ * the matrix-core GEMMs read, enqueued on stream.  The packed matrix has the
+ * same size, N K elements.  It is a sequence of 1 KB tiles, tile (n / 16,
+ * s) covering rows 16 (n/16) .. +15 and the s-th 64-byte run of those rows'
+ * K extent (E = 32 bf16 or 16 fp32 elements); tiles are ordered row block
+ * major.  Inside a tile, element (n, k) with k = s E + e sits in 16-byte
+ * unit 16 (e / (E/4)) + n % 16 at position e % (E/4): one wave-wide 16-byte
+ * load per lane fetches a tile whole.  Requirements: N % 16 == 0 and
+ * K * element size % 128 == 0 (SD_EINVAL otherwise); src and dst must not
+ * overlap.  Used once per weight matrix before sd_init. */
+int sd_pack_linear(const void *src, void *dst, int N, int K, int dtype,
+                   void *stream);
 
 /* Sizes (host-only queries; 0 on an invalid configuration). */
 size_t sd_kv_pool_bytes(const sd_config *cfg, int draft);

@@ -19,7 +19,8 @@ SD_DTYPE_BF16, SD_DTYPE_F32 = 0, 1
 # the symbols include/sd.h declares (checked by the CPU test suite)
 EXPORTS = ("sd_kv_pool_bytes", "sd_workspace_bytes", "sd_init", "sd_prefill", "sd_release",
            "sd_draft_step", "sd_verify", "sd_accept_resample", "sd_kv_commit", "sd_slot_state",
-           "sd_check", "sd_profile", "sd_profile_read", "sd_destroy", "sd_strerror", "sd_last_error")
+           "sd_check", "sd_profile", "sd_profile_read", "sd_destroy", "sd_strerror", "sd_last_error",
+           "sd_pack_linear")
 
 
 class ModelCfg(C.Structure):
@@ -89,6 +90,7 @@ def lib():
         "sd_destroy": (None, [P]),
         "sd_strerror": (C.c_char_p, [I]),
         "sd_last_error": (C.c_char_p, []),
+        "sd_pack_linear": (I, [P, P, I, I, I, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)

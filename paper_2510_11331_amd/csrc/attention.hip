@@ -241,7 +241,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
 
   auto emit = [&](int qi, float val) {
     const int row = row0 + qi / G, h = kvh * G + qi % G;
-    Store<T>::store((T*)p.out, (size_t)row * Hq + h * HD + dd, val);
+    Store<T>::store((T*)p.out, Tile<T>::off(row, h * HD + dd, Hq), val);
   };
 
   if (p.splits == 1) {
@@ -499,15 +499,18 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
     __syncthreads();
   }
   const bool owner = wave_on && kg == 0 && qvalid;
-  bf16_t* out = (bf16_t*)p.out + (size_t)qrow * p.H * HD + (size_t)qh * HD;
+  // four consecutive output dimensions of this lane's query, MFMA-tile layout
+  auto emit4 = [&](int d, float a0, float a1, float a2, float a3) {
+    const size_t off = Tile<bf16_t>::off(qrow, qh * HD + 16 * d + 4 * g, p.H * HD);
+    *(uint2*)((bf16_t*)p.out + off) = make_uint2((uint32_t)f2bf(a0) | ((uint32_t)f2bf(a1) << 16),
+                                                 (uint32_t)f2bf(a2) | ((uint32_t)f2bf(a3) << 16));
+  };
 
   if (p.splits == 1) {
     if (owner) {
       const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
 #pragma unroll
-      for (int d = 0; d < DT; ++d)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) out[16 * d + 4 * g + v] = f2bf(o[d][v] * inv);
+      for (int d = 0; d < DT; ++d) emit4(d, o[d][0] * inv, o[d][1] * inv, o[d][2] * inv, o[d][3] * inv);
     }
     return;
   }
@@ -552,9 +555,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
     }
     const float inv = L > 0.f ? 1.0f / L : 0.f;
 #pragma unroll
-    for (int d = 0; d < DT; ++d)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) out[16 * d + 4 * g + v] = f2bf(O[d][v] * inv);
+    for (int d = 0; d < DT; ++d) emit4(d, O[d][0] * inv, O[d][1] * inv, O[d][2] * inv, O[d][3] * inv);
   }
   if (tid == 0) p.counters[rbk] = 0;
 }

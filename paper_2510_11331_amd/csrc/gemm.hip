@@ -4,16 +4,17 @@
 //
 // The pass is bound by streaming W from HBM, so the kernel is organised
 // around that stream:
+//   * W and A are stored in the MFMA-tile layout (W packed once by
+//     sd_pack_linear, A written that way by the producing kernels), so every
+//     fragment load of a wave is one contiguous 1 KB block;
 //   * a workgroup owns one column tile (16*NT output columns = 16*NT rows
-//     of W; NT in {1, 2, 4, 8}, wider tiles re-read the activations less
+//     of W; NT in {1, 2, 4}, wider tiles re-read the activations less
 //     often) and splits K over its KW waves (up to 16); each wave streams its
-//     K slice of the tile's W rows straight into registers, 64-128
-//     contiguous bytes of a row per step, one step ahead of the MFMAs;
-//   * the matching activation fragments A[rows, K slice] are loaded the same
-//     way (they are small and stay in L2), so the main loop has no LDS
-//     traffic and no barriers, and vmcnt only ever waits for the older step;
-//   * the K permutation inside a step is the same for A and W, so a lane
-//     reads 16-32 contiguous bytes of its weight row per step;
+//     K slice of the tile straight into registers, one step group ahead of
+//     the MFMAs;
+//   * the matching activation fragments are loaded the same way (they are
+//     small and stay in L2), so the main loop has no LDS traffic and no
+//     barriers, and vmcnt only ever waits for the older step group;
 //   * bf16: one v_mfma_f32_16x16x32_bf16 per 16-byte unit; fp32: four
 //     v_mfma_f32_16x16x4_f32;
 //   * the KW partial tiles are added in wave order through LDS
@@ -23,6 +24,8 @@
 //   * epilogues: store fp32, add into the fp32 residual stream, or SwiGLU
 //     over interleaved gate/up rows (written in the model dtype).
 #include "sd_internal.h"
+
+#include <algorithm>
 
 namespace sd {
 
@@ -53,41 +56,28 @@ template <int MT, int NT> struct GemmBounds {
   static constexpr int threads = (MT >= 3 || NT >= 4) ? 512 : 1024;
 };
 
-// Lane (r16, g) streams bytes [16 U g, 16 U (g + 1)) of each 64 U-byte step
-// of its weight rows; the activation fragments use the same bytes, so the K
-// permutation inside a step is shared by both operands.  Waves walk their K
-// slice starting at a workgroup-dependent rotation, which spreads the
-// concurrent activation reads of different workgroups over the L2 channels.
+// Both operands are in the MFMA-tile layout (Tile<T>): fragment (tile t,
+// k-step s) of a lane is the 16-byte unit 64 (t * ksteps + s) + lane, so a
+// wave's load of one fragment is a contiguous 1 KB block.  A wave walks its
+// share of the k-steps in groups of U, starting at a workgroup-dependent
+// rotation that spreads concurrent activation reads over the L2 channels.
 template <typename T, int MT, int NT, int U, int EPI>
 __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(GemmParams p) {
-  constexpr int CB = 64 * U;               // bytes of a row per step
   __shared__ float red[4][MT * NT * 4][64];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int KW = blockDim.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const size_t kbytes = (size_t)p.K * sizeof(T);
-  const int total = (int)(kbytes / CB);
-  const int c0 = 0, c1 = total;
-  const int per = (c1 - c0 + KW - 1) / KW;
-  const int wc0 = min(c0 + wave * per, c1), wc1 = min(wc0 + per, c1);
+  const int ksteps = (int)((size_t)p.K * sizeof(T) / 64);
+  const int groups = ksteps / U;   // K * sizeof(T) is a multiple of 64 U (checked by the host)
+  const int per = (groups + KW - 1) / KW;
+  const int wc0 = min(wave * per, groups), wc1 = min(wc0 + per, groups);
   const int nw = wc1 - wc0;
   const int rot = nw > 0 ? (int)((blockIdx.x * 7u) % (unsigned)nw) : 0;
   const int n0 = blockIdx.x * 16 * NT;
   const int m0 = blockIdx.z * MT * 16;
-
-  const unsigned char* wrow[NT];
-#pragma unroll
-  for (int j = 0; j < NT; ++j)
-    wrow[j] = (const unsigned char*)p.W + (size_t)(n0 + 16 * j + r16) * kbytes + g * 16 * U;
-  const unsigned char* arow[MT];
-  bool aval[MT];
-#pragma unroll
-  for (int i = 0; i < MT; ++i) {
-    const int m = m0 + 16 * i + r16;
-    aval[i] = m < p.M;
-    arow[i] = (const unsigned char*)p.A + (size_t)(aval[i] ? m : 0) * kbytes + g * 16 * U;
-  }
+  const u32x4* wp = (const u32x4*)p.W + (size_t)blockIdx.x * NT * ksteps * 64 + lane;
+  const u32x4* ap = (const u32x4*)p.A + (size_t)blockIdx.z * MT * ksteps * 64 + lane;
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -96,19 +86,18 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   u32x4 ws[2][NT][U], as[2][MT][U];
-  auto load = [&]<int S>(int i) {              // i-th step of this wave's slice
+  auto load = [&]<int S>(int i) {              // i-th step group of this wave's share
     int c = wc0 + i + rot;
     if (c >= wc1) c -= nw;
-    const size_t off = (size_t)c * CB;
+    const int s0 = c * U;
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int u = 0; u < U; ++u) ws[S][j][u] = *(const u32x4*)(wrow[j] + off + u * 16);
+      for (int u = 0; u < U; ++u) ws[S][j][u] = wp[((size_t)j * ksteps + s0 + u) * 64];
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
-      for (int u = 0; u < U; ++u)
-        as[S][t][u] = aval[t] ? *(const u32x4*)(arow[t] + off + u * 16) : u32x4{0u, 0u, 0u, 0u};
+      for (int u = 0; u < U; ++u) as[S][t][u] = ap[((size_t)t * ksteps + s0 + u) * 64];
   };
   auto compute = [&]<int S>() {
 #pragma unroll
@@ -170,7 +159,8 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
         const int F = p.N / 2;
 #pragma unroll
         for (int j = 0; j < NT; j += 2)
-          Store<T>::store((T*)p.out_t, (size_t)m * F + n0 / 2 + 8 * j + r16, silu(acc[i][j][v]) * acc[i][j + 1][v]);
+          Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F),
+                          silu(acc[i][j][v]) * acc[i][j + 1][v]);
       } else {
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
@@ -180,6 +170,34 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
         }
       }
     }
+}
+
+// row-major [N, K] -> MFMA-tile layout, one 16-byte unit per thread
+template <typename T>
+__global__ void pack_linear_kernel(const T* src, T* dst, int N, int K) {
+  constexpr int EPL = Tile<T>::EPL, EPK = Tile<T>::EPK;
+  const int ks = K / EPK;
+  const size_t units = (size_t)N * K / EPL;
+  for (size_t u = blockIdx.x * (size_t)blockDim.x + threadIdx.x; u < units; u += (size_t)gridDim.x * blockDim.x) {
+    const int lane = (int)(u % 64);
+    const size_t ts = u / 64;
+    const int s = (int)(ts % ks), t = (int)(ts / ks);
+    const int r = 16 * t + (lane & 15);
+    const int k = s * EPK + (lane >> 4) * EPL;
+    *(uint4*)(dst + u * EPL) = *(const uint4*)(src + (size_t)r * K + k);
+  }
+}
+
+hipError_t launch_pack_linear(int dtype, const void* src, void* dst, int N, int K, hipStream_t s) {
+  const size_t esz = dtype == 0 ? 2 : 4;
+  if (N <= 0 || K <= 0 || N % 16 || ((size_t)K * esz) % 64) return hipErrorInvalidValue;
+  const size_t units = (size_t)N * K * esz / 16;
+  const int blocks = (int)std::min<size_t>((units + 255) / 256, 65536);
+  if (dtype == 0)
+    hipLaunchKernelGGL(pack_linear_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, (const bf16_t*)src, (bf16_t*)dst, N, K);
+  else
+    hipLaunchKernelGGL(pack_linear_kernel<float>, dim3(blocks), dim3(256), 0, s, (const float*)src, (float*)dst, N, K);
+  return hipGetLastError();
 }
 
 template <typename T, int EPI, int NT, int U>
@@ -209,20 +227,20 @@ template <typename T, int EPI>
 static hipError_t launch_nt(int nt, int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s) {
   switch (nt) {
     case 1:
-      if constexpr (EPI != EPI_SWIGLU) return launch_mt<T, EPI, 1, 2>(mt, grid, threads, p, s);
+      if constexpr (EPI != EPI_SWIGLU) return launch_mt<T, EPI, 1, GEMM_U>(mt, grid, threads, p, s);
       return hipErrorInvalidValue;
-    case 2: return launch_mt<T, EPI, 2, 2>(mt, grid, threads, p, s);
-    case 4: return launch_mt<T, EPI, 4, 2>(mt, grid, threads, p, s);
-    case 8: return launch_mt<T, EPI, 8, 1>(mt, grid, threads, p, s);
+    case 2: return launch_mt<T, EPI, 2, GEMM_U>(mt, grid, threads, p, s);
+    case 4: return launch_mt<T, EPI, 4, GEMM_U>(mt, grid, threads, p, s);
     default: return hipErrorInvalidValue;
   }
 }
 
-int gemm_step_bytes(int nt) { return nt == 8 ? 64 : 128; }
-
 hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int grid_z, const GemmParams& p,
                        hipStream_t s) {
   if (kw < 1 || kw > ((mt >= 3 || nt >= 4) ? 8 : 16)) return hipErrorInvalidValue;
+  if (p.N % (16 * nt) || grid_x * 16 * nt != p.N || grid_z * 16 * mt < p.M ||
+      ((size_t)p.K * (dtype == 0 ? 2 : 4)) % GEMM_CHUNK)
+    return hipErrorInvalidValue;
   dim3 grid(grid_x, 1, grid_z);
   const int threads = 64 * kw;
   if (dtype == 0) {

@@ -33,20 +33,21 @@ template <> struct Vec4<bf16_t> {
     return make_float4(bf2f((bf16_t)(u.x & 0xffff)), bf2f((bf16_t)(u.x >> 16)), bf2f((bf16_t)(u.y & 0xffff)),
                        bf2f((bf16_t)(u.y >> 16)));
   }
-  __device__ __forceinline__ static void store(bf16_t* p, int i4, float4 v) {
-    ((uint2*)p)[i4] = make_uint2((uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16),
-                                 (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+  // four consecutive elements at element offset off (a multiple of 4)
+  __device__ __forceinline__ static void store_at(bf16_t* p, size_t off, float4 v) {
+    *(uint2*)(p + off) = make_uint2((uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16),
+                                    (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
   }
 };
 template <> struct Vec4<float> {
   __device__ __forceinline__ static float4 load(const float* p, int i4) { return ((const float4*)p)[i4]; }
-  __device__ __forceinline__ static void store(float* p, int i4, float4 v) { ((float4*)p)[i4] = v; }
+  __device__ __forceinline__ static void store_at(float* p, size_t off, float4 v) { *(float4*)(p + off) = v; }
 };
 
-// out = x / sqrt(mean(x^2) + eps) * gain for a register-resident row
-// (float4 i of the row is v[k] with i = threadIdx.x + 256 k)
+// row r of out (MFMA-tile layout) = x / sqrt(mean(x^2) + eps) * gain for a
+// register-resident row x (float4 i of the row is v[k], i = threadIdx.x + 256 k)
 template <typename T>
-__device__ void norm_store(const float4 (&v)[RV], int d, const T* gain, T* out, float eps, float* red) {
+__device__ void norm_store(const float4 (&v)[RV], int d, const T* gain, T* out, int r, float eps, float* red) {
   const int d4 = d >> 2;
   float ss = 0.f;
 #pragma unroll
@@ -59,8 +60,8 @@ __device__ void norm_store(const float4 (&v)[RV], int d, const T* gain, T* out, 
     const int i = threadIdx.x + 256 * k;
     if (i < d4) {
       const float4 g = Vec4<T>::load(gain, i);
-      Vec4<T>::store(out, i, make_float4(v[k].x * inv * g.x, v[k].y * inv * g.y, v[k].z * inv * g.z,
-                                         v[k].w * inv * g.w));
+      Vec4<T>::store_at(out, Tile<T>::off(r, 4 * i, d),
+                        make_float4(v[k].x * inv * g.x, v[k].y * inv * g.y, v[k].z * inv * g.z, v[k].w * inv * g.w));
     }
   }
 }
@@ -89,7 +90,7 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
       }
       for (int i = threadIdx.x; i < p.d; i += 256) {
         p.x[(size_t)r * p.d + i] = 0.f;
-        Store<T>::store((T*)p.xn, (size_t)r * p.d + i, 0.f);
+        Store<T>::store((T*)p.xn, Tile<T>::off(r, i, p.d), 0.f);
       }
       return;
     }
@@ -135,7 +136,7 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
     const int i = threadIdx.x + 256 * k;
     if (i < d4) x[i] = v[k];
   }
-  norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn + (size_t)r * p.d, p.eps, red);
+  norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn, r, p.eps, red);
 }
 
 template <typename T>
@@ -150,7 +151,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormParams p) {
     const int i = threadIdx.x + 256 * k;
     v[k] = i < d4 ? x[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn + (size_t)r * p.d, p.eps, red);
+  norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn, r, p.eps, red);
 }
 
 hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s) {

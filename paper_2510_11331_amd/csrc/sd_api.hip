@@ -21,7 +21,6 @@ using namespace sd;
 namespace {
 
 constexpr int KV_BLOCK = 16;
-constexpr int MAX_SPLITS = 8;
 
 struct ModelRT {
   sd_model_cfg c{};
@@ -42,10 +41,6 @@ struct Lane {
   int rb_cap = 0;
   float *x = nullptr, *qkv = nullptr, *q = nullptr, *logits = nullptr;
   void *xn = nullptr, *att = nullptr, *hmid = nullptr;
-  float* partial = nullptr;
-  size_t partial_cap = 0;       // floats
-  int* gemm_cnt = nullptr;
-  int gemm_cnt_n = 0;
   float *attn_o = nullptr, *attn_ml = nullptr;
   size_t attn_o_cap = 0, attn_ml_cap = 0;
   int* attn_cnt = nullptr;
@@ -175,6 +170,7 @@ Dims dims_max(const sd_model_cfg& a, const sd_model_cfg* b) {
 // lane buffers; decode_rb = row blocks of a decode pass, qmax_dec = query vectors per row block
 void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int qmax_dec, int splits,
               int logits_rows, int prefill_rb) {
+  rows = (rows + GEMM_MROWS - 1) / GEMM_MROWS * GEMM_MROWS;   // operands are read in whole 64-row blocks
   ln.rows = rows;
   ln.row_tok = al.take<int32_t>(sizeof(int32_t) * rows);
   ln.row_pos = al.take<int32_t>(sizeof(int32_t) * rows);
@@ -188,11 +184,6 @@ void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int q
   ln.att = al.take<void>(D.esz * rows * D.nq);
   ln.hmid = al.take<void>(D.esz * rows * D.F);
   ln.logits = logits_rows ? al.take<float>(sizeof(float) * logits_rows * D.V) : nullptr;
-  const int nmax = std::max(std::max(D.nqkv, D.d), std::max(2 * D.F, D.V));
-  ln.partial_cap = (size_t)MAX_SPLITS * std::min(rows, GEMM_MROWS) * nmax;
-  ln.partial = al.take<float>(sizeof(float) * ln.partial_cap);
-  ln.gemm_cnt_n = nmax / 16 + 1;
-  ln.gemm_cnt = al.take<int>(sizeof(int) * ln.gemm_cnt_n);
   ln.attn_cnt_n = decode_rb * D.KV;
   ln.attn_o_cap = (size_t)ln.attn_cnt_n * splits * qmax_dec * D.hd;
   ln.attn_ml_cap = (size_t)ln.attn_cnt_n * splits * qmax_dec * 2;
@@ -261,43 +252,34 @@ void prof_end(sd_ctx* ctx, hipStream_t s, ProfRec& r) {
 // ---------------------------------------------------------------- GEMM planning
 
 struct GemmPlan {
-  int nt, mt, kw, gx, gz, splits, cps;
+  int nt, mt, kw, gx, gz;
 };
 
 // One column tile of 16*nt columns per workgroup, kw waves splitting K inside
-// it.  Measured on MI355X at M = 40 (7B-shape verify): the widest tile that
-// still leaves ~170+ workgroups is fastest (wider tiles re-read the
-// activations less often), with 4 waves for 128-column tiles and 8 waves
-// otherwise.  K is not split across workgroups: the cross-workgroup
-// reduction needs a device-scope release per workgroup, which costs more
-// than it recovers at these sizes.
-GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, size_t partial_cap) {
-  (void)partial_cap;
+// it.  Measured on MI355X with packed operands at M = 40 and M = 8 (7B-shape
+// verify and draft passes, weights streamed from HBM): SwiGLU gate/up is
+// fastest with 32-column tiles; other projections take the widest tile
+// (64, then 32 columns) that still leaves ~170+ workgroups, else 16; 8 waves
+// per workgroup throughout.  K is not split across workgroups: the
+// cross-workgroup reduction needs a device-scope release per workgroup,
+// which costs more than it recovers at these sizes.
+GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi) {
   GemmPlan g{};
   g.gz = (M + GEMM_MROWS - 1) / GEMM_MROWS;
   g.mt = g.gz > 1 ? 4 : (M + 15) / 16;
-  g.nt = epi == EPI_SWIGLU ? 2 : 1;
-  for (int nt : {8, 4, 2}) {
-    // register file: 48-row tiles take at most 64 columns, 64-row blocks 32
-    if ((g.mt == 4 && nt > 2) || (g.mt == 3 && nt > 4)) continue;
-    if (nt > g.nt && N % (16 * nt) == 0 && N / (16 * nt) >= 170) {
-      g.nt = nt;
-      break;
-    }
-  }
+  if (epi == EPI_SWIGLU) g.nt = 2;
+  else if (g.mt <= 3 && N % 64 == 0 && N / 64 >= 170) g.nt = 4;   // 64-row blocks take at most 32 columns
+  else if (N % 32 == 0 && N / 32 >= 170) g.nt = 2;
+  else g.nt = 1;
   g.gx = N / (16 * g.nt);
-  const int steps = (int)(K * esz / gemm_step_bytes(g.nt));
-  const int kw_max = (g.mt >= 3 || g.nt >= 4) ? 8 : 16;
-  const int kw_pref = g.nt == 8 ? 4 : kw_max;
-  g.kw = std::max(1, std::min(kw_pref, steps / 2));
-  g.splits = 1;
-  g.cps = steps;
+  const int groups = (int)(K * esz / 64) / GEMM_U;   // k-step groups of one wave step
+  g.kw = std::max(1, std::min(8, groups / 2));
   return g;
 }
 
 int gemm(sd_ctx* ctx, Lane& ln, const ModelRT& m, int epi, const void* A, const void* W, int M, int N,
          int K, float* out, int ldo, void* out_t, hipStream_t s, int prof_kind, int prof_kind2) {
-  const GemmPlan g = plan_gemm(M, N, K, m.esz, epi, ln.partial_cap);
+  const GemmPlan g = plan_gemm(M, N, K, m.esz, epi);
   if (N % (16 * g.nt)) return SD_EINVAL;
   GemmParams p{};
   p.A = A;
@@ -805,6 +787,13 @@ void sd_destroy(sd_ctx* ctx) {
     hipEventDestroy(r.b);
   }
   delete ctx;
+}
+
+int sd_pack_linear(const void* src, void* dst, int N, int K, int dtype, void* stream) {
+  if (!src || !dst || N < 16 || K < 1 || (dtype != SD_DTYPE_BF16 && dtype != SD_DTYPE_F32)) return SD_EINVAL;
+  if (N % 16 || ((size_t)K * esize(dtype)) % GEMM_CHUNK) return SD_EINVAL;
+  HIPCHK(launch_pack_linear(dtype == SD_DTYPE_F32 ? 1 : 0, src, dst, N, K, (hipStream_t)stream));
+  return SD_OK;
 }
 
 const char* sd_last_error(void) { return g_last_error; }

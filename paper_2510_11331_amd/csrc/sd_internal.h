@@ -21,6 +21,22 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
   return (bf16_t)(u >> 16);
 }
 
+// MFMA-tile layout of a matrix-product operand X[R, K] (weights R = N,
+// activations R = M rows padded to 16): a k-step is 64 bytes of a row
+// (32 bf16 or 16 fp32); tile (r / 16, k-step s) is 1 KB holding, for lane
+// l = 16 * (k-group) + r % 16, the 16 bytes of row r, k-group (k % step) /
+// (elements per 16 bytes).  Every 16-byte lane load of an operand fragment
+// is then part of one contiguous 1 KB block.
+template <typename T> struct Tile {
+  static constexpr int EPL = 16 / (int)sizeof(T);   // elements per lane unit
+  static constexpr int EPK = 4 * EPL;                // elements per k-step
+  __host__ __device__ __forceinline__ static size_t off(int r, int k, int K) {
+    const int ks = K / EPK;
+    const int lane = ((k % EPK) / EPL) * 16 + (r & 15);
+    return (((size_t)(r >> 4) * ks + k / EPK) * 64 + lane) * EPL + (k % EPL);
+  }
+};
+
 template <typename T> struct Store;
 template <> struct Store<bf16_t> {
   __device__ __forceinline__ static float load(const bf16_t* p, size_t i) { return bf2f(p[i]); }
@@ -53,7 +69,7 @@ struct RowsParams {
   const void* embed;         // [V, d]
   const void* gain;          // [d]
   float* x;                  // [M, d]
-  void* xn;                  // [M, d]
+  void* xn;                  // [M, d] in the MFMA-tile layout
   int d, V, n_slots;
   float eps;
   int32_t* err;
@@ -62,18 +78,18 @@ struct RowsParams {
 struct NormParams {
   const float* x;   // [rows_in, d]
   const void* gain; // [d]
-  void* xn;         // [M, d]
+  void* xn;         // [M, d] in the MFMA-tile layout
   int M, d, src_stride, src_off;  // output row r reads input row r*src_stride + src_off
   float eps;
 };
 
 struct GemmParams {
-  const void* A;      // [M, K] activations
-  const void* W;      // [N, K] weights
+  const void* A;      // [M, K] activations, MFMA-tile layout (rows padded to the M block)
+  const void* W;      // [N, K] weights, MFMA-tile layout
   int M, N, K;
   float* out;         // STORE: out[m * ldo + n]; RESID: out[m * ldo + n] += acc
   int ldo;
-  void* out_t;        // SWIGLU: out_t[m * (N/2) + f]
+  void* out_t;        // SWIGLU: out_t[M, N/2] in the MFMA-tile layout
 };
 
 struct RopeParams {
@@ -100,7 +116,7 @@ struct AttnParams {
   int R, nrb, H, KV, hd;
   int keys_per_split, splits;
   float scale;
-  void* out;                 // [M, H hd] model dtype
+  void* out;                 // [M, H hd] model dtype, MFMA-tile layout
   float* part_o;             // [nrb*KV, splits, Qmax, hd]
   float* part_ml;            // [nrb*KV, splits, Qmax, 2]
   int* counters;             // [nrb*KV]
@@ -161,11 +177,12 @@ hipError_t launch_draft_sample(const DraftSampleParams& p, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
 hipError_t launch_commit(const CommitParams& p, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t s);
+hipError_t launch_pack_linear(int dtype, const void* src, void* dst, int N, int K, hipStream_t s);
 
 // GEMM geometry (shared by host planning and the kernel)
-constexpr int GEMM_CHUNK = 128;        // K dims must be a multiple of this many bytes
+constexpr int GEMM_U = 2;              // 64-byte k-steps per wave step of the GEMM
+constexpr int GEMM_CHUNK = 64 * GEMM_U; // K dims must be a multiple of this many bytes
 constexpr int GEMM_MROWS = 64;         // rows per M block (4 MFMA row tiles)
-int gemm_step_bytes(int nt);           // bytes of a weight row per wave step for tile width nt
 
 // attention geometry
 constexpr int ATTN_KEYS = 64;          // keys per LDS chunk

@@ -41,27 +41,29 @@ def interleave_gate_up(gate: np.ndarray, up: np.ndarray) -> np.ndarray:
 
 class GPUModel:
     """Weights of one model on the device, in libsd's layout: fused QKV rows,
-    gate/up rows interleaved in 16-row blocks."""
+    gate/up rows interleaved in 16-row blocks, and the five projection
+    matrices (QKV, O, gate/up, down, LM head) repacked on the device by
+    sd_pack_linear into the MFMA-tile layout."""
 
     def __init__(self, shape, get: Callable[[str], np.ndarray], device="cuda"):
         self.shape = shape
         self.bf16 = shape.dtype == "bf16"
         self.device = device
         self.keep: List[torch.Tensor] = []
-        up = self._upload
+        up, pk = self._upload, self._packed
         self.embed = up(get("embed"))
-        self.lm_head = up(get("lm_head"))
+        self.lm_head = pk(get("lm_head"))
         self.final_norm = up(get("final_norm"))
         L = shape.n_layers
         self.attn_norm, self.wqkv, self.wo, self.ffn_norm, self.wgu, self.wdown = ([] for _ in range(6))
         for l in range(L):
             p = f"l{l}."
             self.attn_norm.append(up(get(p + "attn_norm")))
-            self.wqkv.append(up(np.concatenate([get(p + "wq"), get(p + "wk"), get(p + "wv")], axis=0)))
-            self.wo.append(up(get(p + "wo")))
+            self.wqkv.append(pk(np.concatenate([get(p + "wq"), get(p + "wk"), get(p + "wv")], axis=0)))
+            self.wo.append(pk(get(p + "wo")))
             self.ffn_norm.append(up(get(p + "ffn_norm")))
-            self.wgu.append(up(interleave_gate_up(get(p + "w_gate"), get(p + "w_up"))))
-            self.wdown.append(up(get(p + "w_down")))
+            self.wgu.append(pk(interleave_gate_up(get(p + "w_gate"), get(p + "w_up"))))
+            self.wdown.append(pk(get(p + "w_down")))
         arr = lambda ts: (C.c_void_p * L)(*[t.data_ptr() for t in ts])
         self._arrays = [arr(self.attn_norm), arr(self.wqkv), arr(self.wo), arr(self.ffn_norm),
                         arr(self.wgu), arr(self.wdown)]
@@ -70,14 +72,30 @@ class GPUModel:
         self.cstruct = _lib.Weights(self.embed.data_ptr(), self.lm_head.data_ptr(), self.final_norm.data_ptr(),
                                     cast(a[0]), cast(a[1]), cast(a[2]), cast(a[3]), cast(a[4]), cast(a[5]))
 
-    def _upload(self, a: np.ndarray) -> torch.Tensor:
+    def _to_device(self, a: np.ndarray) -> torch.Tensor:
         a = np.ascontiguousarray(a)
         if self.bf16:
-            t = torch.from_numpy(a.view(np.int16)).to(self.device).view(torch.bfloat16)
-        else:
-            t = torch.from_numpy(a.astype(np.float32, copy=False)).to(self.device)
+            return torch.from_numpy(a.view(np.int16)).to(self.device).view(torch.bfloat16)
+        return torch.from_numpy(a.astype(np.float32, copy=False)).to(self.device)
+
+    def _upload(self, a: np.ndarray) -> torch.Tensor:
+        t = self._to_device(a)
         self.keep.append(t)
         return t
+
+    def _packed(self, a: np.ndarray) -> torch.Tensor:
+        """[N, K] row-major on the host -> packed on the device."""
+        N, K = a.shape
+        src = self._to_device(a)
+        dst = torch.empty_like(src)
+        stream = torch.cuda.current_stream(src.device).cuda_stream
+        _lib.check(_lib.lib().sd_pack_linear(src.data_ptr(), dst.data_ptr(), N, K,
+                                             _lib.SD_DTYPE_BF16 if self.bf16 else _lib.SD_DTYPE_F32, stream),
+                   "sd_pack_linear")
+        torch.cuda.current_stream(src.device).synchronize()
+        del src
+        self.keep.append(dst)
+        return dst
 
 
 class Batch:
