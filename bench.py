@@ -41,20 +41,76 @@ def parse():
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch size")
     ap.add_argument("--gamma", type=int, default=0, help="override the workload's gamma")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="short eager run for rocprofv3 --pmc: a 1 GiB copy kernel (counter calibration) "
+                         "and two eager steps, no JSON line")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 --pmc counter_collection.csv files of --pmc-pass runs "
+                         "(FETCH_SIZE, then WRITE_SIZE) into profiles/pmc_traffic.json and exit")
     return ap.parse_args()
 
 
-def traffic_from_profiles(kernel_key: str):
-    """HBM bytes per launch of the dominant kernel, from the committed
-    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, copy-kernel scaled),
-    or None when no summary for the current kernel is committed."""
-    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+GATEUP_NAME = "gemm_kernel<unsigned short, 3, 2, 2, 2>"   # bf16 bits, MT=3, NT=2, U=2, SwiGLU epilogue
+COPY_NAME = "neg_kernel"                            # torch.neg over 1 GiB of int16
+COPY_BYTES = 1 << 30
+
+
+def kernel_sources_digest() -> str:
+    """Digest of the sources of the dominant kernel: a counter summary is
+    only valid for the code it was taken on."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "sd_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2510_11331_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles():
+    """HBM bytes per launch of the gate/up GEMM from the committed rocprofv3
+    counter summary (FETCH_SIZE + WRITE_SIZE, each scaled by the copy
+    kernel's reading), or None if there is none for the current sources."""
     try:
-        d = json.load(open(path))
-        e = d.get(kernel_key)
-        return None if e is None else float(e["bytes_per_launch"])
-    except Exception:
+        d = json.load(open(TRAFFIC_JSON))
+        if d.get("sources_digest") != kernel_sources_digest():
+            return None
+        return float(d["gateup"]["bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
         return None
+
+
+def summarise_counters(fetch_csv: str, write_csv: str) -> None:
+    import csv
+
+    def per_kernel(path, counter):
+        vals = {}
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if row.get("Counter_Name") != counter:
+                    continue
+                name = row["Kernel_Name"]
+                key = "copy" if COPY_NAME in name else "gateup" if GATEUP_NAME in name else None
+                if key:
+                    vals.setdefault(key, []).append(float(row["Counter_Value"]))
+        return vals
+
+    fe, wr = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    kib = COPY_BYTES / 1024
+    f_scale = kib / float(np.median(fe["copy"]))
+    w_scale = kib / float(np.median(wr["copy"]))
+    fetch = float(np.median(fe["gateup"])) * f_scale * 1024
+    write = float(np.median(wr["gateup"])) * w_scale * 1024
+    out = {"kernel": GATEUP_NAME + " (target FFN gate/up, M=40, N=22016, K=4096)",
+           "sources_digest": kernel_sources_digest(),
+           "copy_kernel": {"bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES,
+                           "fetch_kib": float(np.median(fe["copy"])), "write_kib": float(np.median(wr["copy"])),
+                           "fetch_scale": f_scale, "write_scale": w_scale},
+           "gateup": {"launches": len(fe["gateup"]), "fetch_kib_raw": float(np.median(fe["gateup"])),
+                      "write_kib_raw": float(np.median(wr["gateup"])),
+                      "fetch_bytes": fetch, "write_bytes": write, "bytes_per_launch": fetch + write}}
+    with open(TRAFFIC_JSON, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out, indent=1))
 
 
 def cpu_baseline(wl, B, gamma, emitted_per_step):
@@ -122,6 +178,9 @@ def cpu_baseline(wl, B, gamma, emitted_per_step):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        summarise_counters(*args.traffic_from)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
               "the single-GPU figure is the per-GPU share of the task-sharded design.", file=sys.stderr)
@@ -152,6 +211,17 @@ def main():
 
     batch = eng.batch(list(range(B)), gamma)
     ut = synth.uniform_table(42, list(range(B)), W + 2 * K, gamma)
+    if args.pmc_pass:
+        src = torch.ones(COPY_BYTES // 2, dtype=torch.int16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        generate(eng, [batch], [ut[:2]], 2, two_streams=False)
+        torch.cuda.synchronize()
+        print("[bench] pmc pass done", file=sys.stderr, flush=True)
+        return
     graph = StepGraph(eng, batch)                  # one HIP graph replays every step
     generate_graph(eng, batch, ut[:W], W, graph)   # warmup
     torch.cuda.synchronize()
@@ -220,10 +290,10 @@ def main():
         "mean_accepted": round(float(acc.mean()), 4),
         "mean_emitted_per_step": round(float((acc + 1).mean()), 4),
         "device_flags": flags,
-        "roofline": {"kernel": "gemm_kernel<bf16, MT=3, NT=2, SWIGLU> (target FFN gate/up, M=40, N=22016, K=4096)",
+        "roofline": {"kernel": GATEUP_NAME + " (target FFN gate/up, M=40, N=22016, K=4096)",
                      "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic_from_profiles("gemm_gateup_7b_b8"),
+                     "traffic": traffic_from_profiles(),
                      "launch_ms": round(gu_ms, 5), "algorithmic_bytes_per_launch": gu_bytes},
         "cpu_baseline": None,
     }

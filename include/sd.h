@@ -82,7 +82,12 @@ typedef struct {
  * The per-layer pointer arrays are host arrays of n_layers device pointers;
  * sd_init copies them.
  *   wqkv  [(n_heads + 2 n_kv_heads) head_dim, d_model]: query rows (head
- *         major), then key rows, then value rows.
+ *         major), then key rows, then value rows.  The rows of each query
+ *         and key head are in rotary pair order: for b < head_dim / 32,
+ *         rows 32b..32b+15 of the head are its dims 16b..16b+15 and rows
+ *         32b+16..32b+31 its dims head_dim/2+16b..+15 (the two halves that
+ *         the rotary embedding rotates together); value rows are in plain
+ *         order.
  *   wo    [d_model, n_heads head_dim]
  *   wgu   [2 d_ffn, d_model]: gate and up rows interleaved in blocks of 16:
  *         rows 32b..32b+15 are gate rows 16b..16b+15, rows 32b+16..32b+31

@@ -1,6 +1,7 @@
-// Rotary embedding + KV append, and causal multi-query attention over the
-// paged KV cache (Section II-A: eq. d_kv grows the cache by concatenation;
-// eq. d_atte / f21 attend with softmax(q K^T / sqrt(d0)) V).
+// Causal multi-query attention over the paged KV cache (Section II-A: eq.
+// d_kv grows the cache by concatenation, done by the QKV projection's
+// epilogue; eq. d_atte / f21 attend with softmax(q K^T / sqrt(d0)) V), and
+// the rotary (cos, sin) table that epilogue reads.
 //
 // Paged layout of one layer's pool, per 16-token block and kv head: K as
 // [16 tokens][hd], V transposed as [hd][16 tokens] (so the P*V operand of a
@@ -24,62 +25,24 @@
 // relative precision.  fp32 models: a vector kernel with K/V staged in LDS.
 #include "sd_internal.h"
 
+#include <algorithm>
+
 namespace sd {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <typename T>
-__global__ __launch_bounds__(256) void rope_append_kernel(RopeParams p) {
-  __shared__ float cs[64], sn[64];
-  const int r = blockIdx.x;
-  const int pos = p.row_pos[r];
-  if (pos < 0) return;
-  const int slot = p.row_slot[r];
-  const int hd = p.hd, half = hd / 2;
-  const int Nq = p.H * hd, Nk = p.KV * hd;
-  const float* src = p.qkv + (size_t)r * (Nq + 2 * Nk);
-  const bool ok = pos < p.state[slot * ST_N + ST_CAP];
-  const int blk = ok ? p.block_table[(size_t)slot * p.mbps + pos / 16] : 0;
-  const int off = pos % 16;
-  T* kv = (T*)p.kv;
-  const size_t kbase = (((size_t)blk * 2 + 0) * p.KV) * 16 * hd + (size_t)off * hd;
-  const size_t vbase = (((size_t)blk * 2 + 1) * p.KV) * 16 * hd + off;
-
-  // angle pos * theta^(-2i/hd) in float64, once per frequency
-  if (threadIdx.x < half) {
-    const int i = threadIdx.x;
-    const double ang = (double)pos * pow(p.theta, -2.0 * (double)i / (double)hd);
-    double sd_, cd_;
-    sincos(ang, &sd_, &cd_);
-    cs[i] = (float)cd_;
-    sn[i] = (float)sd_;
-  }
-  __syncthreads();
-  const int nh = p.H + p.KV;
-  for (int idx = threadIdx.x; idx < nh * half; idx += blockDim.x) {
-    const int i = idx % half, h = idx / half;
-    const float c = cs[i], s = sn[i];
-    if (h < p.H) {
-      const float a = src[h * hd + i], b = src[h * hd + i + half];
-      float* q = p.q + (size_t)r * Nq + h * hd;
-      q[i] = a * c - b * s;
-      q[i + half] = a * s + b * c;
-    } else if (ok) {
-      const int kh = h - p.H;
-      const float a = src[Nq + kh * hd + i], b = src[Nq + kh * hd + i + half];
-      Store<T>::store(kv, kbase + (size_t)kh * 16 * hd + i, a * c - b * s);
-      Store<T>::store(kv, kbase + (size_t)kh * 16 * hd + i + half, a * s + b * c);
-    }
-  }
-  if (ok) {
-    for (int idx = threadIdx.x; idx < Nk; idx += blockDim.x) {
-      const int kh = idx / hd, d = idx % hd;
-      Store<T>::store(kv, vbase + (size_t)kh * 16 * hd + (size_t)d * 16, src[Nq + Nk + idx]);
-    }
-  } else if (threadIdx.x == 0) {
-    atomicOr(p.err, ERR_KV_OVERFLOW);
+// rotary (cos, sin) table: angle pos * theta^(-2i/hd) in float64, rounded to
+// float32 once (the rotation itself is done in float32 by the QKV epilogue)
+__global__ void rope_table_kernel(float2* tab, int n_pos, int half, double theta) {
+  const size_t n = (size_t)n_pos * half;
+  for (size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x; idx < n; idx += (size_t)gridDim.x * blockDim.x) {
+    const int pos = (int)(idx / half), i = (int)(idx % half);
+    const double ang = (double)pos * pow(theta, -2.0 * (double)i / (double)(2 * half));
+    double s, c;
+    sincos(ang, &s, &c);
+    tab[idx] = make_float2((float)c, (float)s);
   }
 }
 
@@ -560,11 +523,11 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
   if (tid == 0) p.counters[rbk] = 0;
 }
 
-hipError_t launch_rope_append(int dtype, const RopeParams& p, hipStream_t s) {
-  if (p.M <= 0) return hipSuccess;
-  if (p.hd > 128) return hipErrorInvalidValue;
-  if (dtype == 0) hipLaunchKernelGGL(rope_append_kernel<bf16_t>, dim3(p.M), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL(rope_append_kernel<float>, dim3(p.M), dim3(256), 0, s, p);
+hipError_t launch_rope_table(float2* tab, int n_pos, int half, double theta, hipStream_t s) {
+  if (n_pos <= 0 || half <= 0) return hipErrorInvalidValue;
+  const size_t n = (size_t)n_pos * half;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(rope_table_kernel, dim3(blocks), dim3(256), 0, s, tab, n_pos, half, theta);
   return hipGetLastError();
 }
 

@@ -21,8 +21,14 @@
 //     (deterministic); K is never split across workgroups (a cross-workgroup
 //     reduction needs a device-scope release per workgroup, which costs more
 //     than it recovers at these sizes);
-//   * epilogues: store fp32, add into the fp32 residual stream, or SwiGLU
-//     over interleaved gate/up rows (written in the model dtype).
+//   * for projections with few column tiles, K may also be split over
+//     gridDim.y workgroups that store fp32 partial sums; the RMSNorm that
+//     follows adds them to the residual stream in split order (no
+//     cross-workgroup synchronisation, deterministic);
+//   * epilogues: store fp32, add into the fp32 residual stream, SwiGLU over
+//     interleaved gate/up rows (written in the model dtype), or, for the QKV
+//     projection, the rotary embedding of q and k over pair-ordered rows
+//     with q stored in fp32 and k, v appended to the paged KV cache.
 #include "sd_internal.h"
 
 #include <algorithm>
@@ -52,9 +58,11 @@ template <> struct Mfma<float> {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
 
+// narrow tiles fit 128 VGPRs and run up to 16 waves; wider ones up to 8
 template <int MT, int NT> struct GemmBounds {
-  static constexpr int threads = (MT >= 3 || NT >= 4) ? 512 : 1024;
+  static constexpr int threads = (MT * NT <= 4 && MT < 4 && NT < 4) ? 1024 : 512;
 };
+int gemm_max_waves(int mt, int nt) { return (mt * nt <= 4 && mt < 4 && nt < 4) ? 16 : 8; }
 
 // Both operands are in the MFMA-tile layout (Tile<T>): fragment (tile t,
 // k-step s) of a lane is the 16-byte unit 64 (t * ksteps + s) + lane, so a
@@ -69,7 +77,10 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
   const int KW = blockDim.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int ksteps = (int)((size_t)p.K * sizeof(T) / 64);
-  const int groups = ksteps / U;   // K * sizeof(T) is a multiple of 64 U (checked by the host)
+  // K * sizeof(T) is a multiple of 64 U (checked by the host); split y of
+  // gridDim.y takes step groups [gb, gb + groups)
+  const int gall = ksteps / U, gsp = (gall + gridDim.y - 1) / gridDim.y;
+  const int gb = min((int)blockIdx.y * gsp, gall), groups = min(gsp, gall - gb);
   const int per = (groups + KW - 1) / KW;
   const int wc0 = min(wave * per, groups), wc1 = min(wc0 + per, groups);
   const int nw = wc1 - wc0;
@@ -89,7 +100,7 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
   auto load = [&]<int S>(int i) {              // i-th step group of this wave's share
     int c = wc0 + i + rot;
     if (c >= wc1) c -= nw;
-    const int s0 = c * U;
+    const int s0 = (gb + c) * U;
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
@@ -119,54 +130,104 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     }
   }
 
-  // wave partials -> wave 0, four waves per round, added in wave order
-  for (int base = 0; base < KW; base += 4) {
-    const int slot = wave - base;
-    if (wave != 0 && slot >= 0 && slot < 4) {
+  // Reduction over the KW wave partials, in a fixed order: waves 4.. fold
+  // into waves 0..3 four at a time (slot w holds wave w + base), then waves
+  // 0..3 publish their sums and every wave finishes the output rows (i, v)
+  // with (4 i + v) % KW == wave, adding the four slots in order.
+  for (int base = 4; base < KW; base += 4) {
+    if (wave >= base && wave < base + 4) {
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
         for (int j = 0; j < NT; ++j)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) red[slot][(i * NT + j) * 4 + v][lane] = acc[i][j][v];
+          for (int v = 0; v < 4; ++v) red[wave - base][(i * NT + j) * 4 + v][lane] = acc[i][j][v];
     }
     __syncthreads();
-    if (wave == 0) {
-      for (int s = 0; s < 4; ++s) {
-        const int w = base + s;
-        if (w == 0 || w >= KW) continue;
+    if (wave < 4 && wave + base < KW) {
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
+      for (int i = 0; i < MT; ++i)
 #pragma unroll
-          for (int j = 0; j < NT; ++j)
+        for (int j = 0; j < NT; ++j)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) acc[i][j][v] += red[s][(i * NT + j) * 4 + v][lane];
-      }
+          for (int v = 0; v < 4; ++v) acc[i][j][v] += red[wave][(i * NT + j) * 4 + v][lane];
     }
     __syncthreads();
   }
-  if (wave != 0) return;
+  const int nslot = min(KW, 4);
+  if (wave < nslot) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) red[wave][(i * NT + j) * 4 + v][lane] = acc[i][j][v];
+  }
+  __syncthreads();
 
-  // accumulator element (i, j, v) is row m0 + 16 i + 4 g + v, column n0 + 16 j + r16
+  // output element (i, j, v) is row m0 + 16 i + 4 g + v, column n0 + 16 j + r16
 #pragma unroll
   for (int i = 0; i < MT; ++i)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
+      if ((4 * i + v) % KW != wave) continue;
       const int m = m0 + 16 * i + 4 * g + v;
       if (m >= p.M) continue;
-      if constexpr (EPI == EPI_SWIGLU) {
+      float o[NT];
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        float t = red[0][(i * NT + j) * 4 + v][lane];
+        for (int w = 1; w < nslot; ++w) t += red[w][(i * NT + j) * 4 + v][lane];
+        o[j] = t;
+      }
+      if constexpr (EPI == EPI_QKV) {
+        const RopeParams& rp = p.rope;
+        const int pos = rp.row_pos[m];
+        if (pos < 0) continue;                  // row without an input (no pending draft token)
+        const int blk = rp.row_blk[m];          // -1: K/V not written (over capacity, flagged)
+        const int hd = rp.hd, half = hd / 2, Nq = rp.H * hd, Nqk = Nq + rp.KV * hd;
+        const int off = pos & 15;
+        T* kv = (T*)rp.kv;
+        const size_t kblk = (size_t)max(blk, 0) * 2 * rp.KV * 16 * hd, vblk = kblk + (size_t)rp.KV * 16 * hd;
+#pragma unroll
+        for (int j = 0; j < NT; j += 2) {
+          const int c0 = n0 + 16 * j;           // pair of 16-row tiles, 32-aligned
+          if (c0 < Nqk) {
+            // tiles j, j+1 hold dims 16b + r16 and hd/2 + 16b + r16 of head h
+            const int h = c0 / hd, d1 = 16 * ((c0 % hd) / 32) + r16, d2 = d1 + half;
+            const float2 cs = rp.tab[(size_t)pos * half + d1];
+            const float a = o[j], b = o[j + 1];
+            const float o1 = a * cs.x - b * cs.y, o2 = a * cs.y + b * cs.x;
+            if (h < rp.H) {
+              float* q = rp.q + (size_t)m * Nq + (size_t)h * hd;
+              q[d1] = o1;
+              q[d2] = o2;
+            } else if (blk >= 0) {
+              const size_t kb = kblk + (size_t)(h - rp.H) * 16 * hd + (size_t)off * hd;
+              Store<T>::store(kv, kb + d1, o1);
+              Store<T>::store(kv, kb + d2, o2);
+            }
+          } else if (blk >= 0) {
+#pragma unroll
+            for (int jj = j; jj < j + 2; ++jj) {
+              const int cv = c0 + 16 * (jj - j) + r16 - Nqk;
+              Store<T>::store(kv, vblk + (size_t)(cv / hd) * 16 * hd + (size_t)(cv % hd) * 16 + off, o[jj]);
+            }
+          }
+        }
+      } else if constexpr (EPI == EPI_SWIGLU) {
         // tiles (2k, 2k+1) are the gate and up rows of the same 16 outputs
         const int F = p.N / 2;
 #pragma unroll
         for (int j = 0; j < NT; j += 2)
-          Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F),
-                          silu(acc[i][j][v]) * acc[i][j + 1][v]);
+          Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F), silu(o[j]) * o[j + 1]);
       } else {
+        const size_t row = EPI == EPI_PART ? (size_t)blockIdx.y * p.M + m : (size_t)m;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
-          float* o = p.out + (size_t)m * p.ldo + n0 + 16 * j + r16;
-          if constexpr (EPI == EPI_RESID) *o += acc[i][j][v];
-          else *o = acc[i][j][v];
+          float* dst = p.out + row * p.ldo + n0 + 16 * j + r16;
+          if constexpr (EPI == EPI_RESID) *dst += o[j];
+          else *dst = o[j];
         }
       }
     }
@@ -227,7 +288,7 @@ template <typename T, int EPI>
 static hipError_t launch_nt(int nt, int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s) {
   switch (nt) {
     case 1:
-      if constexpr (EPI != EPI_SWIGLU) return launch_mt<T, EPI, 1, GEMM_U>(mt, grid, threads, p, s);
+      if constexpr (EPI != EPI_SWIGLU && EPI != EPI_QKV) return launch_mt<T, EPI, 1, GEMM_U>(mt, grid, threads, p, s);
       return hipErrorInvalidValue;
     case 2: return launch_mt<T, EPI, 2, GEMM_U>(mt, grid, threads, p, s);
     case 4: return launch_mt<T, EPI, 4, GEMM_U>(mt, grid, threads, p, s);
@@ -235,21 +296,28 @@ static hipError_t launch_nt(int nt, int mt, dim3 grid, int threads, const GemmPa
   }
 }
 
-hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int grid_z, const GemmParams& p,
-                       hipStream_t s) {
-  if (kw < 1 || kw > ((mt >= 3 || nt >= 4) ? 8 : 16)) return hipErrorInvalidValue;
+hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
+                       const GemmParams& p, hipStream_t s) {
+  if (kw < 1 || kw > gemm_max_waves(mt, nt)) return hipErrorInvalidValue;
   if (p.N % (16 * nt) || grid_x * 16 * nt != p.N || grid_z * 16 * mt < p.M ||
       ((size_t)p.K * (dtype == 0 ? 2 : 4)) % GEMM_CHUNK)
     return hipErrorInvalidValue;
-  dim3 grid(grid_x, 1, grid_z);
+  if (ksplit < 1 || (ksplit > 1 && epi != EPI_PART) || ksplit > (int)((size_t)p.K * (dtype == 0 ? 2 : 4) / GEMM_CHUNK))
+    return hipErrorInvalidValue;
+  dim3 grid(grid_x, ksplit, grid_z);
   const int threads = 64 * kw;
+  if (epi == EPI_QKV && (p.rope.hd % 32 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd)) return hipErrorInvalidValue;
   if (dtype == 0) {
     if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, p, s);
     if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, p, s);
+    if (epi == EPI_QKV) return launch_nt<bf16_t, EPI_QKV>(nt, mt, grid, threads, p, s);
+    if (epi == EPI_PART) return launch_nt<bf16_t, EPI_PART>(nt, mt, grid, threads, p, s);
     return launch_nt<bf16_t, EPI_SWIGLU>(nt, mt, grid, threads, p, s);
   }
   if (epi == EPI_STORE) return launch_nt<float, EPI_STORE>(nt, mt, grid, threads, p, s);
   if (epi == EPI_RESID) return launch_nt<float, EPI_RESID>(nt, mt, grid, threads, p, s);
+  if (epi == EPI_QKV) return launch_nt<float, EPI_QKV>(nt, mt, grid, threads, p, s);
+  if (epi == EPI_PART) return launch_nt<float, EPI_PART>(nt, mt, grid, threads, p, s);
   return launch_nt<float, EPI_SWIGLU>(nt, mt, grid, threads, p, s);
 }
 

@@ -87,6 +87,7 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
         p.row_tok[r] = 0;
         p.row_pos[r] = -1;
         p.row_slot[r] = 0;
+        p.row_blk[r] = -1;
       }
       for (int i = threadIdx.x; i < p.d; i += 256) {
         p.x[(size_t)r * p.d + i] = 0.f;
@@ -117,6 +118,16 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
       p.row_slot[r] = slot;
     }
   }
+  if (threadIdx.x == 0) {
+    // KV block of this row for every layer of the pass; a write beyond the
+    // slot's capacity is skipped and flagged
+    int blk = -1;
+    if (pos >= 0) {
+      if (pos < p.state[(size_t)slot * ST_N + ST_CAP]) blk = p.block_table[(size_t)slot * p.mbps + pos / 16];
+      else atomicOr(p.err, ERR_KV_OVERFLOW);
+    }
+    p.row_blk[r] = blk;
+  }
   if (pos >= 0 && (tok < 0 || tok >= p.V)) {
     if (threadIdx.x == 0) atomicOr(p.err, ERR_BAD_TOKEN);
     tok = 0;
@@ -143,13 +154,36 @@ template <typename T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(NormParams p) {
   __shared__ float red[4];
   const int r = blockIdx.x;
-  const float4* x = (const float4*)(p.x + ((size_t)r * p.src_stride + p.src_off) * p.d);
+  const size_t rin = (size_t)r * p.src_stride + p.src_off;
+  float4* x = (float4*)(p.x + rin * p.d);
   const int d4 = p.d >> 2;
   float4 v[RV];
 #pragma unroll
   for (int k = 0; k < RV; ++k) {
     const int i = threadIdx.x + 256 * k;
     v[k] = i < d4 ? x[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if (p.part) {
+    // residual add of the K-split partial sums of the preceding projection
+    for (int sp = 0; sp < p.nsplit; ++sp) {
+      const float4* pp = (const float4*)(p.part + ((size_t)sp * p.rows_in + rin) * p.d);
+#pragma unroll
+      for (int k = 0; k < RV; ++k) {
+        const int i = threadIdx.x + 256 * k;
+        if (i < d4) {
+          const float4 a = pp[i];
+          v[k].x += a.x;
+          v[k].y += a.y;
+          v[k].z += a.z;
+          v[k].w += a.w;
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < RV; ++k) {
+      const int i = threadIdx.x + 256 * k;
+      if (i < d4) x[i] = v[k];
+    }
   }
   norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn, r, p.eps, red);
 }

@@ -21,6 +21,7 @@ using namespace sd;
 namespace {
 
 constexpr int KV_BLOCK = 16;
+constexpr int MAX_KSPLIT = 4;   // K splits of a residual projection (partial sums in the workspace)
 
 struct ModelRT {
   sd_model_cfg c{};
@@ -29,6 +30,8 @@ struct ModelRT {
   std::vector<const void*> attn_norm, wqkv, wo, ffn_norm, wgu, wdown;
   unsigned char* pool = nullptr;
   int n_blocks = 0;
+  float2* rope_tab = nullptr;   // [rope_pos, head_dim/2] rotary (cos, sin), in the workspace
+  int rope_pos = 0;
   size_t layer_bytes = 0;   // bytes of one layer's pool
   int nqkv() const { return (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; }
   int nq() const { return c.n_heads * c.head_dim; }
@@ -37,10 +40,12 @@ struct ModelRT {
 
 struct Lane {
   int rows = 0;                 // row capacity
-  int32_t *row_tok = nullptr, *row_pos = nullptr, *row_slot = nullptr, *rowblocks = nullptr;
+  int32_t *row_tok = nullptr, *row_pos = nullptr, *row_slot = nullptr, *row_blk = nullptr, *rowblocks = nullptr;
   int rb_cap = 0;
-  float *x = nullptr, *qkv = nullptr, *q = nullptr, *logits = nullptr;
+  float *x = nullptr, *q = nullptr, *logits = nullptr;
   void *xn = nullptr, *att = nullptr, *hmid = nullptr;
+  float* part = nullptr;        // [MAX_KSPLIT, part_rows, d] K-split partial sums
+  int part_rows = 0;
   float *attn_o = nullptr, *attn_ml = nullptr;
   size_t attn_o_cap = 0, attn_ml_cap = 0;
   int* attn_cnt = nullptr;
@@ -175,14 +180,16 @@ void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int q
   ln.row_tok = al.take<int32_t>(sizeof(int32_t) * rows);
   ln.row_pos = al.take<int32_t>(sizeof(int32_t) * rows);
   ln.row_slot = al.take<int32_t>(sizeof(int32_t) * rows);
+  ln.row_blk = al.take<int32_t>(sizeof(int32_t) * rows);
   ln.rb_cap = prefill_rb;
   ln.rowblocks = al.take<int32_t>(sizeof(int32_t) * 2 * std::max(1, prefill_rb));
   ln.x = al.take<float>(sizeof(float) * rows * D.d);
   ln.xn = al.take<void>(D.esz * rows * D.d);
-  ln.qkv = al.take<float>(sizeof(float) * rows * D.nqkv);
   ln.q = al.take<float>(sizeof(float) * rows * D.nq);
   ln.att = al.take<void>(D.esz * rows * D.nq);
   ln.hmid = al.take<void>(D.esz * rows * D.F);
+  ln.part_rows = std::min(rows, GEMM_MROWS);
+  ln.part = al.take<float>(sizeof(float) * MAX_KSPLIT * ln.part_rows * D.d);
   ln.logits = logits_rows ? al.take<float>(sizeof(float) * logits_rows * D.V) : nullptr;
   ln.attn_cnt_n = decode_rb * D.KV;
   ln.attn_o_cap = (size_t)ln.attn_cnt_n * splits * qmax_dec * D.hd;
@@ -208,6 +215,8 @@ size_t layout(const sd_config* c, sd_ctx* ctx) {
   int32_t* bt_t = al.take<int32_t>(sizeof(int32_t) * (size_t)c->max_slots * mbps);
   int32_t* bt_d = al.take<int32_t>(sizeof(int32_t) * (size_t)c->max_slots * mbps);
   int32_t* err = al.take<int32_t>(sizeof(int32_t) * 4);
+  float2* tab_t = al.take<float2>(sizeof(float2) * (size_t)mbps * KV_BLOCK * (c->target.head_dim / 2));
+  float2* tab_d = al.take<float2>(sizeof(float2) * (size_t)mbps * KV_BLOCK * (c->draft.head_dim / 2));
   const int kps = keys_per_split(c->max_ctx);
   const int splits = (c->max_ctx + kps - 1) / kps;
   const Dims Dt = dims_max(c->target, &c->draft);
@@ -224,6 +233,9 @@ size_t layout(const sd_config* c, sd_ctx* ctx) {
     ctx->bt_t = bt_t;
     ctx->bt_d = bt_d;
     ctx->err = err;
+    ctx->tgt.rope_tab = tab_t;
+    ctx->dft.rope_tab = tab_d;
+    ctx->tgt.rope_pos = ctx->dft.rope_pos = mbps * KV_BLOCK;
     ctx->lv = lv;
     ctx->ld = ld;
     ctx->keys_per_split = kps;
@@ -252,35 +264,66 @@ void prof_end(sd_ctx* ctx, hipStream_t s, ProfRec& r) {
 // ---------------------------------------------------------------- GEMM planning
 
 struct GemmPlan {
-  int nt, mt, kw, gx, gz;
+  int nt, mt, kw, gx, ksplit, gz;
 };
 
 // One column tile of 16*nt columns per workgroup, kw waves splitting K inside
-// it.  Measured on MI355X with packed operands at M = 40 and M = 8 (7B-shape
-// verify and draft passes, weights streamed from HBM): SwiGLU gate/up is
-// fastest with 32-column tiles; other projections take the widest tile
-// (64, then 32 columns) that still leaves ~170+ workgroups, else 16; 8 waves
-// per workgroup throughout.  K is not split across workgroups: the
-// cross-workgroup reduction needs a device-scope release per workgroup,
-// which costs more than it recovers at these sizes.
-GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi) {
+// it.  Chosen from sweeps on MI355X with packed operands at M = 40 and M = 8
+// (7B-shape verify and draft passes, weights streamed from HBM):
+//   * SwiGLU gate/up: 32-column tiles, 8 waves;
+//   * QKV and LM head: 64-column tiles with 6 waves when that leaves ~170+
+//     workgroups, else 32-column tiles with 8 waves (QKV needs an even
+//     number of tiles for the rotary pairs);
+//   * residual projections (O, down), M <= 64 with an RMSNorm after them
+//     (split_ok): few column tiles, so K is split over workgroups until
+//     there are ~256 of them (32-column tiles at M > 16); the partial sums
+//     go through the workspace to the RMSNorm, which adds them to the
+//     residual stream.  Without split_ok the output is added in place.
+// K is never split with a cross-workgroup reduction inside the GEMM: that
+// needs a device-scope release per workgroup, which costs more than it saves.
+GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = false) {
   GemmPlan g{};
   g.gz = (M + GEMM_MROWS - 1) / GEMM_MROWS;
   g.mt = g.gz > 1 ? 4 : (M + 15) / 16;
-  if (epi == EPI_SWIGLU) g.nt = 2;
-  else if (g.mt <= 3 && N % 64 == 0 && N / 64 >= 170) g.nt = 4;   // 64-row blocks take at most 32 columns
-  else if (N % 32 == 0 && N / 32 >= 170) g.nt = 2;
-  else g.nt = 1;
-  g.gx = N / (16 * g.nt);
+  g.ksplit = 1;
+  g.kw = 8;
   const int groups = (int)(K * esz / 64) / GEMM_U;   // k-step groups of one wave step
-  g.kw = std::max(1, std::min(8, groups / 2));
+  if (epi == EPI_SWIGLU) {
+    g.nt = 2;
+  } else if (epi == EPI_RESID && split_ok && g.gz == 1) {
+    g.nt = (g.mt >= 2 && N % 32 == 0) ? 2 : 1;
+    const int gx = N / (16 * g.nt);
+    g.ksplit = std::min(std::min(MAX_KSPLIT, std::max(1, (256 + gx - 1) / gx)), std::max(1, groups / 4));
+    if (g.ksplit == 1 && g.nt == 2) g.nt = 1;
+  } else if (g.mt <= 3 && N % 64 == 0 && N / 64 >= 170) {
+    g.nt = 4;                                         // 64-row blocks take at most 32 columns
+    g.kw = 6;
+  } else if (N % 32 == 0 && (N / 32 >= 170 || epi == EPI_QKV)) {
+    g.nt = 2;
+  } else {
+    g.nt = 1;
+  }
+  g.gx = N / (16 * g.nt);
+  const int gps = (groups + g.ksplit - 1) / g.ksplit;
+  g.kw = std::max(1, std::min(g.kw, gps / 2));
   return g;
 }
 
-int gemm(sd_ctx* ctx, Lane& ln, const ModelRT& m, int epi, const void* A, const void* W, int M, int N,
-         int K, float* out, int ldo, void* out_t, hipStream_t s, int prof_kind, int prof_kind2) {
-  const GemmPlan g = plan_gemm(M, N, K, m.esz, epi);
+// Launch one projection.  part != null allows the K-split form for EPI_RESID:
+// then *nsplit receives the number of partial sums written to part
+// ([nsplit, M, ldo]) instead of being added to out, and the caller's RMSNorm
+// adds them; otherwise *nsplit = 0.
+int gemm(sd_ctx* ctx, const ModelRT& m, int epi, const void* A, const void* W, int M, int N, int K,
+         float* out, int ldo, void* out_t, hipStream_t s, int prof_kind, int prof_kind2,
+         const RopeParams* rope = nullptr, float* part = nullptr, int* nsplit = nullptr) {
+  GemmPlan g = plan_gemm(M, N, K, m.esz, epi, part != nullptr);
   if (N % (16 * g.nt)) return SD_EINVAL;
+  if (nsplit) *nsplit = 0;
+  if (g.ksplit > 1) {
+    epi = EPI_PART;
+    out = part;
+    if (nsplit) *nsplit = g.ksplit;
+  }
   GemmParams p{};
   p.A = A;
   p.W = W;
@@ -290,13 +333,16 @@ int gemm(sd_ctx* ctx, Lane& ln, const ModelRT& m, int epi, const void* A, const 
   p.out = out;
   p.ldo = ldo;
   p.out_t = out_t;
+  if (rope) p.rope = *rope;
   const double out_bytes = epi == EPI_SWIGLU ? (double)M * (N / 2) * m.esz
+                           : epi == EPI_QKV  ? (double)M * (m.nq() * 4 + (N - m.nq()) * m.esz)
+                           : epi == EPI_PART ? (double)M * N * 4 * g.ksplit
                                              : (double)M * N * 4 * (epi == EPI_RESID ? 2 : 1);
   const double bytes = (double)N * K * m.esz + (double)M * K * m.esz + out_bytes;
   ProfRec r1, r2;
   prof_begin(ctx, s, r1, prof_kind, bytes);
   prof_begin(ctx, s, r2, prof_kind2, bytes);
-  HIPCHK(launch_gemm(m.c.dtype == SD_DTYPE_F32 ? 1 : 0, epi, g.nt, g.mt, g.kw, g.gx, g.gz, p, s));
+  HIPCHK(launch_gemm(m.c.dtype == SD_DTYPE_F32 ? 1 : 0, epi, g.nt, g.mt, g.kw, g.gx, g.ksplit, g.gz, p, s));
   prof_end(ctx, s, r2);
   prof_end(ctx, s, r1);
   return SD_OK;
@@ -322,31 +368,27 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
   rows.row_tok = ln.row_tok;
   rows.row_pos = ln.row_pos;
   rows.row_slot = ln.row_slot;
+  rows.row_blk = ln.row_blk;
+  rows.block_table = bt;
+  rows.mbps = ctx->mbps;
   rows.state = ctx->state;
   rows.err = ctx->err;
   rows.n_slots = ctx->cfg.max_slots;
   HIPCHK(launch_rows_embed(dt, rows, s));
   const int pk_all = verify ? SD_PROF_GEMM_VERIFY_ALL : -1;
+  int ns = 0;                   // K-split partial sums pending in ln.part
   for (int l = 0; l < c.n_layers; ++l) {
-    int rc = gemm(ctx, ln, m, EPI_STORE, ln.xn, m.wqkv[l], M, m.nqkv(), d, ln.qkv, m.nqkv(), nullptr, s,
-                  pk_all, -1);
-    if (rc) return rc;
     RopeParams rp{};
-    rp.qkv = ln.qkv;
     rp.q = ln.q;
     rp.kv = m.pool + (size_t)l * m.layer_bytes;
+    rp.tab = m.rope_tab;
     rp.row_pos = ln.row_pos;
-    rp.row_slot = ln.row_slot;
-    rp.block_table = bt;
-    rp.state = ctx->state;
-    rp.M = M;
+    rp.row_blk = ln.row_blk;
     rp.H = c.n_heads;
     rp.KV = c.n_kv_heads;
     rp.hd = c.head_dim;
-    rp.mbps = ctx->mbps;
-    rp.theta = c.rope_theta;
-    rp.err = ctx->err;
-    HIPCHK(launch_rope_append(dt, rp, s));
+    int rc = gemm(ctx, m, EPI_QKV, ln.xn, m.wqkv[l], M, m.nqkv(), d, nullptr, 0, nullptr, s, pk_all, -1, &rp);
+    if (rc) return rc;
     AttnParams ap{};
     ap.q = ln.q;
     ap.kv = rp.kv;
@@ -360,13 +402,14 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.H = c.n_heads;
     ap.KV = c.n_kv_heads;
     ap.hd = c.head_dim;
-    // split the keys only when the (row block, kv head) items alone leave the
-    // chip idle: a split costs a device-scope release per workgroup
+    // split the keys only when the (row block, kv head) items leave more than
+    // half of the 256 compute units idle: a split costs a device-scope release
+    // per workgroup, which on MI355X (measured at 128 items, 8-wave
+    // workgroups) costs more than the idle units
     int splits = attn_splits;
-    if (splits > 1) {
-      const int items = nrb * c.n_kv_heads;
-      splits = std::min(splits, std::max(1, (256 + items - 1) / items));
-    }
+    const int items = nrb * c.n_kv_heads;
+    if (items >= 128) splits = 1;
+    else if (splits > 1) splits = std::min(splits, std::max(1, (256 + items - 1) / items));
     const int kps = (ctx->cfg.max_ctx + 63) / 64 * 64;
     ap.splits = splits;
     ap.keys_per_split = splits > 1 ? std::max(ctx->keys_per_split, (kps / splits + 63) / 64 * 64) : kps;
@@ -381,24 +424,31 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     prof_begin(ctx, s, ra, verify ? SD_PROF_ATTN_VERIFY : -1, 0);
     HIPCHK(launch_attention(dt, ap, s));
     prof_end(ctx, s, ra);
-    rc = gemm(ctx, ln, m, EPI_RESID, ln.att, m.wo[l], M, d, m.nq(), ln.x, d, nullptr, s, pk_all, -1);
+    // residual projections may leave K-split partial sums in ln.part for the
+    // RMSNorm after them to add
+    const bool can_split = M <= ln.part_rows;
+    rc = gemm(ctx, m, EPI_RESID, ln.att, m.wo[l], M, d, m.nq(), ln.x, d, nullptr, s, pk_all, -1, nullptr,
+              can_split ? ln.part : nullptr, &ns);
     if (rc) return rc;
-    NormParams np{ln.x, m.ffn_norm[l], ln.xn, M, d, 1, 0, c.rms_eps};
+    NormParams np{ln.x, ns ? ln.part : nullptr, ns, m.ffn_norm[l], ln.xn, M, d, 1, 0, M, c.rms_eps};
     HIPCHK(launch_rmsnorm(dt, np, s));
-    rc = gemm(ctx, ln, m, EPI_SWIGLU, ln.xn, m.wgu[l], M, 2 * c.d_ffn, d, nullptr, 0, ln.hmid, s, pk_all,
+    rc = gemm(ctx, m, EPI_SWIGLU, ln.xn, m.wgu[l], M, 2 * c.d_ffn, d, nullptr, 0, ln.hmid, s, pk_all,
               verify ? SD_PROF_GEMM_VERIFY_GATEUP : -1);
     if (rc) return rc;
-    rc = gemm(ctx, ln, m, EPI_RESID, ln.hmid, m.wdown[l], M, d, c.d_ffn, ln.x, d, nullptr, s, pk_all, -1);
+    const bool norm_next = l + 1 < c.n_layers || lm_M > 0;
+    rc = gemm(ctx, m, EPI_RESID, ln.hmid, m.wdown[l], M, d, c.d_ffn, ln.x, d, nullptr, s, pk_all, -1, nullptr,
+              can_split && norm_next ? ln.part : nullptr, &ns);
     if (rc) return rc;
     if (l + 1 < c.n_layers) {
-      NormParams nn{ln.x, m.attn_norm[l + 1], ln.xn, M, d, 1, 0, c.rms_eps};
+      NormParams nn{ln.x, ns ? ln.part : nullptr, ns, m.attn_norm[l + 1], ln.xn, M, d, 1, 0, M, c.rms_eps};
       HIPCHK(launch_rmsnorm(dt, nn, s));
     }
   }
   if (lm_M > 0) {
-    NormParams fn{ln.x, m.final_norm, ln.xn, lm_M, d, lm_stride, lm_off, c.rms_eps};
+    NormParams fn{ln.x, ns ? ln.part : nullptr, ns, m.final_norm, ln.xn, lm_M, d, lm_stride, lm_off, M,
+                  c.rms_eps};
     HIPCHK(launch_rmsnorm(dt, fn, s));
-    int rc = gemm(ctx, ln, m, EPI_STORE, ln.xn, m.lm_head, lm_M, c.vocab, d, logits, c.vocab, nullptr, s,
+    int rc = gemm(ctx, m, EPI_STORE, ln.xn, m.lm_head, lm_M, c.vocab, d, logits, c.vocab, nullptr, s,
                   pk_all, -1);
     if (rc) return rc;
   }
@@ -470,9 +520,14 @@ int sd_init(const sd_config* cfg, const sd_weights* target, const sd_weights* dr
   ctx->slots.resize(cfg->max_slots);
   for (int b = cfg->kv_blocks_target - 1; b >= 0; --b) ctx->free_t.push_back(b);
   for (int b = cfg->kv_blocks_draft - 1; b >= 0; --b) ctx->free_d.push_back(b);
-  // device state: zero counters, invalid slots, no errors (fill kernels, synchronous here)
+  // device state: zero counters, invalid slots, no errors; rotary tables
+  // (kernels, synchronous here)
   hipStream_t s = nullptr;
   bool ok = launch_fill_i32((int32_t*)cfg->workspace, 0, layout(cfg, nullptr) / 4, s) == hipSuccess &&
+            launch_rope_table(ctx->tgt.rope_tab, ctx->tgt.rope_pos, cfg->target.head_dim / 2,
+                              cfg->target.rope_theta, s) == hipSuccess &&
+            launch_rope_table(ctx->dft.rope_tab, ctx->dft.rope_pos, cfg->draft.head_dim / 2,
+                              cfg->draft.rope_theta, s) == hipSuccess &&
             hipStreamSynchronize(s) == hipSuccess;
   if (!ok) {
     delete ctx;

@@ -66,6 +66,9 @@ struct RowsParams {
   int32_t* row_tok;          // [M]
   int32_t* row_pos;          // [M]; -1 = inactive row
   int32_t* row_slot;         // [M]
+  int32_t* row_blk;          // [M] KV block the row's K/V go to; -1 = none (inactive, or over capacity)
+  const int32_t* block_table;  // [slots, mbps] of the model run over the rows
+  int mbps;
   const void* embed;         // [V, d]
   const void* gain;          // [d]
   float* x;                  // [M, d]
@@ -76,11 +79,28 @@ struct RowsParams {
 };
 
 struct NormParams {
-  const float* x;   // [rows_in, d]
-  const void* gain; // [d]
-  void* xn;         // [M, d] in the MFMA-tile layout
+  float* x;           // [rows_in, d] residual stream
+  const float* part;  // null, or [nsplit, rows_in, d] partial sums added to x first (in split order)
+  int nsplit;
+  const void* gain;   // [d]
+  void* xn;           // [M, d] in the MFMA-tile layout
   int M, d, src_stride, src_off;  // output row r reads input row r*src_stride + src_off
+  int rows_in;
   float eps;
+};
+
+
+// Rotary embedding (rotate-half pairs (i, i + hd/2), angle pos * theta^(-2i/hd))
+// and KV append, done by the epilogue of the QKV projection.  Query and key
+// rows of the fused weight are in pair order (see sd_weights), so the two
+// halves of a pair meet in one lane.
+struct RopeParams {
+  float* q;                    // [M, H hd] fp32, rotary applied
+  void* kv;                    // layer base of the pool: [blocks, 2, KV, 16, hd], V blocks as [hd][16]
+  const float2* tab;           // [positions, hd/2] (cos, sin), fp64 angles rounded to fp32
+  const int32_t* row_pos;      // [M]; -1 = inactive row
+  const int32_t* row_blk;      // [M] KV block of the row's position; -1 = not written
+  int H, KV, hd;
 };
 
 struct GemmParams {
@@ -90,19 +110,7 @@ struct GemmParams {
   float* out;         // STORE: out[m * ldo + n]; RESID: out[m * ldo + n] += acc
   int ldo;
   void* out_t;        // SWIGLU: out_t[M, N/2] in the MFMA-tile layout
-};
-
-struct RopeParams {
-  const float* qkv;   // [M, (H + 2KV) hd]
-  float* q;           // [M, H hd]
-  void* kv;           // layer base of the pool: [blocks, 2, KV, 16, hd]
-  const int32_t* row_pos;
-  const int32_t* row_slot;
-  const int32_t* block_table;  // [slots, mbps]
-  const int32_t* state;
-  int M, H, KV, hd, mbps;
-  double theta;
-  int32_t* err;
+  RopeParams rope;    // QKV: rotary embedding of q and k, K/V appended to the cache
 };
 
 struct AttnParams {
@@ -161,16 +169,20 @@ struct CommitParams {
   int32_t* err;
 };
 
-enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+// PART: K split over gridDim.y workgroups; split y stores its partial sum to
+// out[(y * M + m) * ldo + n], the residual add happens in the next RMSNorm
+enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_PART = 4 };
 
 // ---------------------------------------------------------------- launchers
 // dtype: 0 bf16, 1 fp32 (same values as SD_DTYPE_*)
 
 hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s);
 hipError_t launch_rmsnorm(int dtype, const NormParams& p, hipStream_t s);
-hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int grid_z,
+int gemm_max_waves(int mt, int nt);   // waves per workgroup the (mt, nt) tile allows
+hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
                        const GemmParams& p, hipStream_t s);
-hipError_t launch_rope_append(int dtype, const RopeParams& p, hipStream_t s);
+// tab[pos * half + i] = (cos, sin) of pos * theta^(-i/half), pos < n_pos, i < half
+hipError_t launch_rope_table(float2* tab, int n_pos, int half, double theta, hipStream_t s);
 hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s);
 hipError_t launch_softmax(const SoftmaxParams& p, hipStream_t s);
 hipError_t launch_draft_sample(const DraftSampleParams& p, hipStream_t s);

@@ -39,9 +39,19 @@ def interleave_gate_up(gate: np.ndarray, up: np.ndarray) -> np.ndarray:
     return np.stack([gate.reshape(F // 16, 16, d), up.reshape(F // 16, 16, d)], axis=1).reshape(2 * F, d)
 
 
+def rotary_pair_order(w: np.ndarray, head_dim: int) -> np.ndarray:
+    """[heads * hd, d] query or key rows -> the same rows with each head in
+    rotary pair order: for b < hd/32, rows 32b..32b+15 are dims 16b..16b+15
+    and rows 32b+16..32b+31 are dims hd/2+16b..hd/2+16b+15."""
+    n, d = w.shape
+    h = w.reshape(n // head_dim, 2, head_dim // 32, 16, d)      # [head, half, b, 16, d]
+    return np.ascontiguousarray(h.transpose(0, 2, 1, 3, 4)).reshape(n, d)
+
+
 class GPUModel:
-    """Weights of one model on the device, in libsd's layout: fused QKV rows,
-    gate/up rows interleaved in 16-row blocks, and the five projection
+    """Weights of one model on the device, in libsd's layout: fused QKV rows
+    (query and key heads in rotary pair order), gate/up rows interleaved in
+    16-row blocks, and the five projection
     matrices (QKV, O, gate/up, down, LM head) repacked on the device by
     sd_pack_linear into the MFMA-tile layout."""
 
@@ -59,7 +69,9 @@ class GPUModel:
         for l in range(L):
             p = f"l{l}."
             self.attn_norm.append(up(get(p + "attn_norm")))
-            self.wqkv.append(pk(np.concatenate([get(p + "wq"), get(p + "wk"), get(p + "wv")], axis=0)))
+            hd = shape.head_dim
+            self.wqkv.append(pk(np.concatenate([rotary_pair_order(get(p + "wq"), hd),
+                                                rotary_pair_order(get(p + "wk"), hd), get(p + "wv")], axis=0)))
             self.wo.append(pk(get(p + "wo")))
             self.ffn_norm.append(up(get(p + "ffn_norm")))
             self.wgu.append(pk(interleave_gate_up(get(p + "w_gate"), get(p + "w_up"))))
