@@ -3,10 +3,12 @@
 // epilogue; eq. d_atte / f21 attend with softmax(q K^T / sqrt(d0)) V), and
 // the rotary (cos, sin) table that epilogue reads.
 //
-// Paged layout of one layer's pool, per 16-token block and kv head: K as
-// [16 tokens][hd], V transposed as [hd][16 tokens] (so the P*V operand of a
-// matrix instruction is 4 consecutive tokens of one dimension); a slot's
-// block table maps position / 16 to a block.
+// Paged layout of one layer's pool, per 16-token block and kv head: K in the
+// layout of the S = K Q^T matrix instruction for bf16 (kv_key_off: every
+// wave load of a key k-step is a contiguous 1 KB) or as [16 tokens][hd] for
+// fp32, V transposed as [hd][16 tokens] (so the P*V operand of a matrix
+// instruction is 4 consecutive tokens of one dimension); a slot's block
+// table maps position / 16 to a block.
 //
 // Attention work item = (row block, kv head, key split).  A row block is a
 // run of consecutive rows of one task (the gamma+1 verify rows of a task, its
@@ -20,7 +22,8 @@
 //
 // bf16 models: S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_16x16x32_bf16,
 // 16 query vectors per wave, keys streamed from the cache straight into
-// registers 32 at a time (two blocks), one step ahead; q and p enter the
+// registers 32 at a time (two blocks), one step ahead, with non-temporal
+// loads (each cache byte is read once per pass); q and p enter the
 // matrix instruction as bf16 hi + lo pairs, which keeps them at ~2^-16
 // relative precision.  fp32 models: a vector kernel with K/V staged in LDS.
 #include "sd_internal.h"
@@ -32,6 +35,7 @@ namespace sd {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // rotary (cos, sin) table: angle pos * theta^(-2i/hd) in float64, rounded to
 // float32 once (the rotation itself is done in float32 by the QKV epilogue)
@@ -57,11 +61,8 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// the vector kernel serves fp32 caches only (bf16 runs on the matrix kernel)
 template <typename T> struct KvT;
-template <> struct KvT<bf16_t> {
-  static constexpr int KST_PAD = 2;   // K row stride hd+2 elements: 32-bit reads hit distinct banks
-  static constexpr int EPU = 8;       // elements per 16-byte unit
-};
 template <> struct KvT<float> {
   static constexpr int KST_PAD = 1;
   static constexpr int EPU = 4;
@@ -275,18 +276,17 @@ __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
                                                  c, 0, 0, 0);
 }
 
-// Wave w of a workgroup (8 waves) takes query tile w % QTe (16 query
+// Wave w of a workgroup (WAVES = 8) takes query tile w % QTe (16 query
 // vectors) and key group w / QTe: 32-key steps kb = k_begin + 32 (kg + KG j).
 // Lane (r16, g): query r16 of the tile; in S^T it holds keys 4g..4g+3 of
 // both blocks of the step, in O^T dimensions 16 dt + 4g .. +3.
-constexpr int ATTN_WAVES = 8;
-
-template <int HD>
-__global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnParams p) {
+template <int HD, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p) {
   constexpr int UPG = HD / 32;             // 16-byte K units per lane group (HD/4 dims)
   constexpr int DT = HD / 16;              // 16-dimension output tiles
-  __shared__ float s_o[4][16][HD + 4];        // one slot per query tile
-  __shared__ float s_m[4][16], s_l[4][16];
+  constexpr int NSLOT = WAVES / 2;         // merge slots: half the waves hand over in the first round
+  __shared__ float s_o[NSLOT][16][HD + 4];
+  __shared__ float s_m[NSLOT][16], s_l[NSLOT][16];
   __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -306,7 +306,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
   const int Qn = nr * G;
   const int QT = (Qn + 15) >> 4;
   const int QTe = QT == 3 ? 4 : QT;
-  const int KG = ATTN_WAVES / QTe;
+  const int KG = WAVES / QTe;
   const int qt = wave % QTe, kg = wave / QTe;
   const bool wave_on = qt < QT;
 
@@ -342,7 +342,10 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
   const bf16_t* kv = (const bf16_t*)p.kv;
   const int32_t* bt = p.block_table + (size_t)slot * p.mbps;
   const size_t blk_stride = (size_t)2 * p.KV * 16 * HD;
-  const size_t koff = (size_t)kvh * 16 * HD + (size_t)r16 * HD + g * (HD / 4);
+  // key block in the matrix-instruction layout: k-step s is the 1 KB run at
+  // unit 64 s, this lane's 16 bytes at unit 64 s + lane (token r16, dims
+  // g HD/4 + 8 s .. + 8)
+  const size_t koff = (size_t)kvh * 16 * HD + (size_t)lane * 8;
   const size_t voff = (size_t)p.KV * 16 * HD + (size_t)kvh * 16 * HD + (size_t)r16 * 16 + 4 * g;
 
   // two register stages of one 32-key step: K rows (two blocks) and V^T quads
@@ -356,7 +359,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
       const bool ok = bi < p.mbps && kb + 16 * t < k_end;
       const bf16_t* base = kv + (size_t)(ok ? bt[bi] : 0) * blk_stride;
 #pragma unroll
-      for (int s = 0; s < UPG; ++s) Kf[S][t][s] = *(const u32x4*)(base + koff + 8 * s);
+      for (int s = 0; s < UPG; ++s) Kf[S][t][s] = __builtin_nontemporal_load((const u32x4*)(base + koff + 512 * s));
       // keys at or past k_end were never written: their scores are masked, and
       // their V entries are zeroed so that p = 0 never meets a NaN/Inf pattern
       const int nq = min(max(k_end - (kb + 16 * t + 4 * g), 0), 4);
@@ -364,7 +367,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
       const uint32_t my = nq >= 4 ? 0xffffffffu : (nq == 3 ? 0xffffu : 0u);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const uint2 v = *(const uint2*)(base + voff + (size_t)d * 256);
+        const u32x2 v = __builtin_nontemporal_load((const u32x2*)(base + voff + (size_t)d * 256));
         Vf[S][t][d][0] = v.x & mx;
         Vf[S][t][d][1] = v.y & my;
       }
@@ -432,23 +435,24 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
     }
   }
 
-  // merge the key groups of a query tile into key group 0, in key-group
-  // order: in round k, key group k hands its state over through the slot of
-  // its query tile
-  for (int k = 1; k < KG; ++k) {
-    if (wave_on && kg == k) {
+  // merge the key groups of each query tile into key group 0 as a binary
+  // tree (fixed order): in the round of stride h, key group kg with
+  // kg % 2h == h hands its state to kg - h through slot qt KG/2 + kg / 2h
+  for (int h = 1; h < KG; h *= 2) {
+    const int sl = qt * (KG / 2) + kg / (2 * h);
+    if (wave_on && kg % (2 * h) == h) {
       if (g == 0) {
-        s_m[qt][r16] = m_run;
-        s_l[qt][r16] = l_run;
+        s_m[sl][r16] = m_run;
+        s_l[sl][r16] = l_run;
       }
 #pragma unroll
       for (int d = 0; d < DT; ++d)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) s_o[qt][r16][16 * d + 4 * g + v] = o[d][v];
+        for (int v = 0; v < 4; ++v) s_o[sl][r16][16 * d + 4 * g + v] = o[d][v];
     }
     __syncthreads();
-    if (wave_on && kg == 0) {
-      const float mb = s_m[qt][r16], lb = s_l[qt][r16];
+    if (wave_on && kg % (2 * h) == 0) {
+      const float mb = s_m[sl][r16], lb = s_l[sl][r16];
       const float M = fmaxf(m_run, mb);
       const float a = m_run == -INFINITY ? 0.f : expf(m_run - M);
       const float b = mb == -INFINITY ? 0.f : expf(mb - M);
@@ -456,7 +460,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void attention_mfma_kernel(AttnPar
 #pragma unroll
       for (int d = 0; d < DT; ++d)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) o[d][v] = o[d][v] * a + s_o[qt][r16][16 * d + 4 * g + v] * b;
+        for (int v = 0; v < 4; ++v) o[d][v] = o[d][v] * a + s_o[sl][r16][16 * d + 4 * g + v] * b;
       m_run = M;
     }
     __syncthreads();
@@ -551,8 +555,8 @@ hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s) {
   if (p.keys_per_split % 64) return hipErrorInvalidValue;
   const dim3 grid(p.nrb * p.KV, p.splits);
   if (dtype == 0) {
-    if (p.hd == 64) hipLaunchKernelGGL(attention_mfma_kernel<64>, grid, dim3(64 * ATTN_WAVES), 0, s, p);
-    else if (p.hd == 128) hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(64 * ATTN_WAVES), 0, s, p);
+    if (p.hd == 64) hipLaunchKernelGGL((attention_mfma_kernel<64, 8>), grid, dim3(64 * 8), 0, s, p);
+    else if (p.hd == 128) hipLaunchKernelGGL((attention_mfma_kernel<128, 8>), grid, dim3(64 * 8), 0, s, p);
     else return hipErrorInvalidValue;
     return hipGetLastError();
   }

@@ -96,19 +96,26 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  bool arow[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) arow[t] = m0 + 16 * t + r16 < p.M;
   u32x4 ws[2][NT][U], as[2][MT][U];
   auto load = [&]<int S>(int i) {              // i-th step group of this wave's share
     int c = wc0 + i + rot;
     if (c >= wc1) c -= nw;
     const int s0 = (gb + c) * U;
+    // weights are read once: non-temporal loads keep them from evicting the
+    // activations, which every workgroup re-reads from L2
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int u = 0; u < U; ++u) ws[S][j][u] = wp[((size_t)j * ksteps + s0 + u) * 64];
+      for (int u = 0; u < U; ++u) ws[S][j][u] = __builtin_nontemporal_load(&wp[((size_t)j * ksteps + s0 + u) * 64]);
+    // activation rows at or past M are padding: not loaded (their outputs are dropped)
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
-      for (int u = 0; u < U; ++u) as[S][t][u] = ap[((size_t)t * ksteps + s0 + u) * 64];
+      for (int u = 0; u < U; ++u)
+        as[S][t][u] = arow[t] ? ap[((size_t)t * ksteps + s0 + u) * 64] : u32x4{0u, 0u, 0u, 0u};
   };
   auto compute = [&]<int S>() {
 #pragma unroll
@@ -203,9 +210,9 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
               q[d1] = o1;
               q[d2] = o2;
             } else if (blk >= 0) {
-              const size_t kb = kblk + (size_t)(h - rp.H) * 16 * hd + (size_t)off * hd;
-              Store<T>::store(kv, kb + d1, o1);
-              Store<T>::store(kv, kb + d2, o2);
+              const size_t kb = kblk + (size_t)(h - rp.H) * 16 * hd;
+              Store<T>::store(kv, kb + kv_key_off<T>(off, d1, hd), o1);
+              Store<T>::store(kv, kb + kv_key_off<T>(off, d2, hd), o2);
             }
           } else if (blk >= 0) {
 #pragma unroll

@@ -150,7 +150,9 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
   norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn, r, p.eps, red);
 }
 
-template <typename T>
+// NS: number of K-split partial sums to add into the residual row first (all
+// loads are issued before the first add; the adds follow split order)
+template <typename T, int NS>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(NormParams p) {
   __shared__ float red[4];
   const int r = blockIdx.x;
@@ -158,29 +160,26 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormParams p) {
   float4* x = (float4*)(p.x + rin * p.d);
   const int d4 = p.d >> 2;
   float4 v[RV];
+  float4 a[NS > 0 ? NS : 1][RV];
 #pragma unroll
   for (int k = 0; k < RV; ++k) {
     const int i = threadIdx.x + 256 * k;
     v[k] = i < d4 ? x[i] : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-  if (p.part) {
-    // residual add of the K-split partial sums of the preceding projection
-    for (int sp = 0; sp < p.nsplit; ++sp) {
-      const float4* pp = (const float4*)(p.part + ((size_t)sp * p.rows_in + rin) * p.d);
 #pragma unroll
-      for (int k = 0; k < RV; ++k) {
-        const int i = threadIdx.x + 256 * k;
-        if (i < d4) {
-          const float4 a = pp[i];
-          v[k].x += a.x;
-          v[k].y += a.y;
-          v[k].z += a.z;
-          v[k].w += a.w;
-        }
-      }
-    }
+    for (int sp = 0; sp < NS; ++sp)
+      a[sp][k] = i < d4 ? ((const float4*)(p.part + ((size_t)sp * p.rows_in + rin) * p.d))[i]
+                        : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if constexpr (NS > 0) {
 #pragma unroll
     for (int k = 0; k < RV; ++k) {
+#pragma unroll
+      for (int sp = 0; sp < NS; ++sp) {
+        v[k].x += a[sp][k].x;
+        v[k].y += a[sp][k].y;
+        v[k].z += a[sp][k].z;
+        v[k].w += a[sp][k].w;
+      }
       const int i = threadIdx.x + 256 * k;
       if (i < d4) x[i] = v[k];
     }
@@ -196,12 +195,25 @@ hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int NS>
+static hipError_t launch_norm_ns(int dtype, const NormParams& p, hipStream_t s) {
+  if (dtype == 0) hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, NS>), dim3(p.M), dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((rmsnorm_kernel<float, NS>), dim3(p.M), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_rmsnorm(int dtype, const NormParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
   if ((p.d & 3) || p.d > 256 * 4 * RV) return hipErrorInvalidValue;
-  if (dtype == 0) hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(p.M), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(p.M), dim3(256), 0, s, p);
-  return hipGetLastError();
+  const int ns = p.part ? p.nsplit : 0;
+  switch (ns) {
+    case 0: return launch_norm_ns<0>(dtype, p, s);
+    case 1: return launch_norm_ns<1>(dtype, p, s);
+    case 2: return launch_norm_ns<2>(dtype, p, s);
+    case 3: return launch_norm_ns<3>(dtype, p, s);
+    case 4: return launch_norm_ns<4>(dtype, p, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 __global__ void fill_i32_kernel(int32_t* p, int32_t v, size_t n) {

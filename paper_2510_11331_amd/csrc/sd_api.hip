@@ -204,6 +204,7 @@ void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int q
 int prefill_qb(const sd_model_cfg& m) {
   const int G = m.n_heads / m.n_kv_heads;
   int qb = std::max(1, ATTN_QMAX / G);
+  if (m.dtype == SD_DTYPE_BF16) return qb;   // the matrix kernel's LDS does not grow with the rows
   while (qb > 1 && attention_lds_bytes(m.head_dim, esize(m.dtype), qb * G) > 64 * 1024) --qb;
   return qb;
 }

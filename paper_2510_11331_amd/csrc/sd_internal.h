@@ -27,6 +27,20 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
 // l = 16 * (k-group) + r % 16, the 16 bytes of row r, k-group (k % step) /
 // (elements per 16 bytes).  Every 16-byte lane load of an operand fragment
 // is then part of one contiguous 1 KB block.
+// Element offset of key (token t, dim d) inside one 16-token block of one kv
+// head.  bf16 caches use the layout of the attention's matrix instruction:
+// for each of the hd/32 k-steps s, a 1 KB run of 64 16-byte units, unit
+// 16 g + t holding dims g (hd/4) + 8 s .. + 8 (g < 4), so every key load of
+// a wave is contiguous.  fp32 caches are token-major ([16][hd]).
+template <typename T> __host__ __device__ __forceinline__ int kv_key_off(int t, int d, int hd) {
+  if constexpr (sizeof(T) == 2) {
+    const int q = hd / 4, g = d / q, s = (d % q) / 8;
+    return ((s * 4 + g) * 16 + t) * 8 + (d & 7);
+  } else {
+    return t * hd + d;
+  }
+}
+
 template <typename T> struct Tile {
   static constexpr int EPL = 16 / (int)sizeof(T);   // elements per lane unit
   static constexpr int EPK = 4 * EPL;                // elements per k-step
