@@ -205,10 +205,14 @@ int sd_slot_state(sd_ctx *ctx, int B, const int32_t *slots, int32_t *out,
  * skipped).  Synchronises the stream; clears the flags. */
 int sd_check(sd_ctx *ctx, void *stream, int32_t *flags_out);
 
-/* Kernel timing with HIP events on the launch stream (off by default).
- * kind: SD_PROF_* below.  sd_profile_read synchronises the recorded events
- * and returns the number of timed launches and their summed milliseconds;
- * reading resets the counters. */
+/* Timing with HIP events (off by default).  kind: SD_PROF_* below.  The
+ * GEMM and attention kinds time each kernel with start/stop events that its
+ * own dispatch timestamps (kernel begin to end, the interval a profiler
+ * reports); the VERIFY and DRAFT kinds time the whole call with events
+ * recorded on its stream.  bytes: algorithmic HBM bytes of the timed GEMMs
+ * (weights + activations read + outputs written).  sd_profile_read
+ * synchronises the recorded events and returns the number of timed
+ * intervals, their summed milliseconds and bytes; reading resets that kind. */
 enum {
     SD_PROF_GEMM_VERIFY_GATEUP = 0,   /* target FFN gate/up GEMM (+SwiGLU)  */
     SD_PROF_GEMM_VERIFY_ALL = 1,      /* every target GEMM in sd_verify     */

@@ -536,7 +536,7 @@ hipError_t launch_rope_table(float2* tab, int n_pos, int half, double theta, hip
 }
 
 template <typename T, int HD>
-static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s) {
+static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const size_t lds = attn_lds_bytes(HD, sizeof(T), p.qmax);
   static size_t attr_bytes = 64 * 1024;     // launches above the default limit raise it first
   if (lds > attr_bytes) {
@@ -545,23 +545,23 @@ static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr_bytes = lds;
   }
-  hipLaunchKernelGGL((attention_kernel<T, HD>), dim3(p.nrb * p.KV, p.splits), dim3(256), lds, s, p);
+  launch_k(attention_kernel<T, HD>, dim3(p.nrb * p.KV, p.splits), dim3(256), (uint32_t)lds, s, e0, e1, p);
   return hipGetLastError();
 }
 
-hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s) {
+hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (p.nrb <= 0) return hipSuccess;
   if (p.qmax > ATTN_QMAX) return hipErrorInvalidValue;
   if (p.keys_per_split % 64) return hipErrorInvalidValue;
   const dim3 grid(p.nrb * p.KV, p.splits);
   if (dtype == 0) {
-    if (p.hd == 64) hipLaunchKernelGGL((attention_mfma_kernel<64, 8>), grid, dim3(64 * 8), 0, s, p);
-    else if (p.hd == 128) hipLaunchKernelGGL((attention_mfma_kernel<128, 8>), grid, dim3(64 * 8), 0, s, p);
+    if (p.hd == 64) launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1, p);
+    else if (p.hd == 128) launch_k(attention_mfma_kernel<128, 8>, grid, dim3(64 * 8), 0, s, e0, e1, p);
     else return hipErrorInvalidValue;
     return hipGetLastError();
   }
-  if (p.hd == 64) return launch_attn_t<float, 64>(p, s);
-  if (p.hd == 128) return launch_attn_t<float, 128>(p, s);
+  if (p.hd == 64) return launch_attn_t<float, 64>(p, s, e0, e1);
+  if (p.hd == 128) return launch_attn_t<float, 128>(p, s, e0, e1);
   return hipErrorInvalidValue;
 }
 

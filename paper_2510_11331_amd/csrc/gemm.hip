@@ -269,20 +269,21 @@ hipError_t launch_pack_linear(int dtype, const void* src, void* dst, int N, int 
 }
 
 template <typename T, int EPI, int NT, int U>
-static hipError_t launch_mt(int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s) {
+static hipError_t launch_mt(int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s, hipEvent_t e0,
+                            hipEvent_t e1) {
   switch (mt) {
-    case 1: hipLaunchKernelGGL((gemm_kernel<T, 1, NT, U, EPI>), grid, dim3(threads), 0, s, p); break;
-    case 2: hipLaunchKernelGGL((gemm_kernel<T, 2, NT, U, EPI>), grid, dim3(threads), 0, s, p); break;
+    case 1: launch_k(gemm_kernel<T, 1, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p); break;
+    case 2: launch_k(gemm_kernel<T, 2, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p); break;
     case 3:
       if constexpr (NT <= 4) {
-        hipLaunchKernelGGL((gemm_kernel<T, 3, NT, U, EPI>), grid, dim3(threads), 0, s, p);
+        launch_k(gemm_kernel<T, 3, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p);
         break;
       }
       return hipErrorInvalidValue;
     case 4:
       // 64-row blocks (prefill) only with tiles of up to 32 columns
       if constexpr (NT <= 2) {
-        hipLaunchKernelGGL((gemm_kernel<T, 4, NT, U, EPI>), grid, dim3(threads), 0, s, p);
+        launch_k(gemm_kernel<T, 4, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p);
         break;
       }
       return hipErrorInvalidValue;
@@ -292,19 +293,20 @@ static hipError_t launch_mt(int mt, dim3 grid, int threads, const GemmParams& p,
 }
 
 template <typename T, int EPI>
-static hipError_t launch_nt(int nt, int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s) {
+static hipError_t launch_nt(int nt, int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s, hipEvent_t e0,
+                            hipEvent_t e1) {
   switch (nt) {
     case 1:
-      if constexpr (EPI != EPI_SWIGLU && EPI != EPI_QKV) return launch_mt<T, EPI, 1, GEMM_U>(mt, grid, threads, p, s);
+      if constexpr (EPI != EPI_SWIGLU && EPI != EPI_QKV) return launch_mt<T, EPI, 1, GEMM_U>(mt, grid, threads, p, s, e0, e1);
       return hipErrorInvalidValue;
-    case 2: return launch_mt<T, EPI, 2, GEMM_U>(mt, grid, threads, p, s);
-    case 4: return launch_mt<T, EPI, 4, GEMM_U>(mt, grid, threads, p, s);
+    case 2: return launch_mt<T, EPI, 2, GEMM_U>(mt, grid, threads, p, s, e0, e1);
+    case 4: return launch_mt<T, EPI, 4, GEMM_U>(mt, grid, threads, p, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
-                       const GemmParams& p, hipStream_t s) {
+                       const GemmParams& p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (kw < 1 || kw > gemm_max_waves(mt, nt)) return hipErrorInvalidValue;
   if (p.N % (16 * nt) || grid_x * 16 * nt != p.N || grid_z * 16 * mt < p.M ||
       ((size_t)p.K * (dtype == 0 ? 2 : 4)) % GEMM_CHUNK)
@@ -315,17 +317,17 @@ hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, i
   const int threads = 64 * kw;
   if (epi == EPI_QKV && (p.rope.hd % 32 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd)) return hipErrorInvalidValue;
   if (dtype == 0) {
-    if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, p, s);
-    if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, p, s);
-    if (epi == EPI_QKV) return launch_nt<bf16_t, EPI_QKV>(nt, mt, grid, threads, p, s);
-    if (epi == EPI_PART) return launch_nt<bf16_t, EPI_PART>(nt, mt, grid, threads, p, s);
-    return launch_nt<bf16_t, EPI_SWIGLU>(nt, mt, grid, threads, p, s);
+    if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, p, s, e0, e1);
+    if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, p, s, e0, e1);
+    if (epi == EPI_QKV) return launch_nt<bf16_t, EPI_QKV>(nt, mt, grid, threads, p, s, e0, e1);
+    if (epi == EPI_PART) return launch_nt<bf16_t, EPI_PART>(nt, mt, grid, threads, p, s, e0, e1);
+    return launch_nt<bf16_t, EPI_SWIGLU>(nt, mt, grid, threads, p, s, e0, e1);
   }
-  if (epi == EPI_STORE) return launch_nt<float, EPI_STORE>(nt, mt, grid, threads, p, s);
-  if (epi == EPI_RESID) return launch_nt<float, EPI_RESID>(nt, mt, grid, threads, p, s);
-  if (epi == EPI_QKV) return launch_nt<float, EPI_QKV>(nt, mt, grid, threads, p, s);
-  if (epi == EPI_PART) return launch_nt<float, EPI_PART>(nt, mt, grid, threads, p, s);
-  return launch_nt<float, EPI_SWIGLU>(nt, mt, grid, threads, p, s);
+  if (epi == EPI_STORE) return launch_nt<float, EPI_STORE>(nt, mt, grid, threads, p, s, e0, e1);
+  if (epi == EPI_RESID) return launch_nt<float, EPI_RESID>(nt, mt, grid, threads, p, s, e0, e1);
+  if (epi == EPI_QKV) return launch_nt<float, EPI_QKV>(nt, mt, grid, threads, p, s, e0, e1);
+  if (epi == EPI_PART) return launch_nt<float, EPI_PART>(nt, mt, grid, threads, p, s, e0, e1);
+  return launch_nt<float, EPI_SWIGLU>(nt, mt, grid, threads, p, s, e0, e1);
 }
 
 }  // namespace sd

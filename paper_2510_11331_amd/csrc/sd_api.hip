@@ -57,10 +57,14 @@ struct Slot {
   std::vector<int> tblocks, dblocks;
 };
 
+// One timed interval: either the span of a whole call (events recorded on
+// the stream around it) or one kernel (events stamped by its own dispatch),
+// counted under every kind in the mask.
 struct ProfRec {
-  int kind;
-  hipEvent_t a, b;
-  double bytes;
+  unsigned mask = 0;
+  bool kernel = false;
+  hipEvent_t a = nullptr, b = nullptr;
+  double bytes = 0;
 };
 
 }  // namespace
@@ -76,7 +80,6 @@ struct sd_ctx {
   std::vector<int> free_t, free_d;
   bool prof = false;
   std::vector<ProfRec> recs;
-  std::vector<ProfRec> done;
 };
 
 namespace {
@@ -247,18 +250,31 @@ size_t layout(const sd_config* c, sd_ctx* ctx) {
 
 // ---------------------------------------------------------------- profiling
 
-void prof_begin(sd_ctx* ctx, hipStream_t s, ProfRec& r, int kind, double bytes) {
-  r.kind = -1;
-  if (!ctx->prof || kind < 0) return;
+// kinds < 0 are ignored; kernel = true: r.a / r.b go to the kernel's launch
+void prof_begin(sd_ctx* ctx, hipStream_t s, ProfRec& r, int kind, int kind2, double bytes, bool kernel) {
+  r = ProfRec{};
+  unsigned mask = (kind >= 0 ? 1u << kind : 0u) | (kind2 >= 0 ? 1u << kind2 : 0u);
+  if (!ctx->prof || !mask) return;
   if (hipEventCreate(&r.a) != hipSuccess) return;
-  if (hipEventCreate(&r.b) != hipSuccess) { hipEventDestroy(r.a); return; }
-  if (hipEventRecord(r.a, s) != hipSuccess) { hipEventDestroy(r.a); hipEventDestroy(r.b); return; }
-  r.kind = kind;
+  if (hipEventCreate(&r.b) != hipSuccess) {
+    hipEventDestroy(r.a);
+    r.a = nullptr;
+    return;
+  }
+  if (!kernel && hipEventRecord(r.a, s) != hipSuccess) {
+    hipEventDestroy(r.a);
+    hipEventDestroy(r.b);
+    r.a = r.b = nullptr;
+    return;
+  }
+  r.mask = mask;
+  r.kernel = kernel;
   r.bytes = bytes;
 }
+
 void prof_end(sd_ctx* ctx, hipStream_t s, ProfRec& r) {
-  if (r.kind < 0) return;
-  hipEventRecord(r.b, s);
+  if (!r.mask) return;
+  if (!r.kernel) hipEventRecord(r.b, s);
   ctx->recs.push_back(r);
 }
 
@@ -340,11 +356,10 @@ int gemm(sd_ctx* ctx, const ModelRT& m, int epi, const void* A, const void* W, i
                            : epi == EPI_PART ? (double)M * N * 4 * g.ksplit
                                              : (double)M * N * 4 * (epi == EPI_RESID ? 2 : 1);
   const double bytes = (double)N * K * m.esz + (double)M * K * m.esz + out_bytes;
-  ProfRec r1, r2;
-  prof_begin(ctx, s, r1, prof_kind, bytes);
-  prof_begin(ctx, s, r2, prof_kind2, bytes);
-  HIPCHK(launch_gemm(m.c.dtype == SD_DTYPE_F32 ? 1 : 0, epi, g.nt, g.mt, g.kw, g.gx, g.ksplit, g.gz, p, s));
-  prof_end(ctx, s, r2);
+  ProfRec r1;
+  prof_begin(ctx, s, r1, prof_kind, prof_kind2, bytes, true);
+  HIPCHK(launch_gemm(m.c.dtype == SD_DTYPE_F32 ? 1 : 0, epi, g.nt, g.mt, g.kw, g.gx, g.ksplit, g.gz, p, s, r1.a,
+                     r1.b));
   prof_end(ctx, s, r1);
   return SD_OK;
 }
@@ -422,8 +437,8 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.counters = ln.attn_cnt;
     ap.qmax = qmax;
     ProfRec ra;
-    prof_begin(ctx, s, ra, verify ? SD_PROF_ATTN_VERIFY : -1, 0);
-    HIPCHK(launch_attention(dt, ap, s));
+    prof_begin(ctx, s, ra, verify ? SD_PROF_ATTN_VERIFY : -1, -1, 0, true);
+    HIPCHK(launch_attention(dt, ap, s, ra.a, ra.b));
     prof_end(ctx, s, ra);
     // residual projections may leave K-split partial sums in ln.part for the
     // RMSNorm after them to add
@@ -702,7 +717,7 @@ int sd_draft_step(sd_ctx* ctx, int B, const int32_t* slots, int gamma, int i, co
   rp.slots = slots;
   rp.draft_tok = draft_tok;
   ProfRec pr;
-  prof_begin(ctx, s, pr, SD_PROF_DRAFT, 0);
+  prof_begin(ctx, s, pr, SD_PROF_DRAFT, -1, 0, false);
   int rc = forward(ctx, m, ln, rp, M, B, nullptr, R, ctx->attn_splits, R * m.G(), B, R, R - 1, ln.logits,
                    ctx->bt_d, false, s);
   if (rc) return rc;
@@ -738,7 +753,7 @@ int sd_verify(sd_ctx* ctx, int B, const int32_t* slots, int gamma, const int32_t
   rp.draft_tok = draft_tok;
   float* z = logits ? logits : p;
   ProfRec pr;
-  prof_begin(ctx, s, pr, SD_PROF_VERIFY, 0);
+  prof_begin(ctx, s, pr, SD_PROF_VERIFY, -1, 0, false);
   int rc = forward(ctx, m, ln, rp, M, B, nullptr, R, ctx->attn_splits, R * m.G(), M, 1, 0, z, ctx->bt_t,
                    true, s);
   if (rc) return rc;
@@ -816,7 +831,7 @@ int sd_profile_read(sd_ctx* ctx, int kind, int64_t* count, double* ms, double* b
   double t = 0, by = 0;
   std::vector<ProfRec> keep;
   for (ProfRec& r : ctx->recs) {
-    if (r.kind != kind) {
+    if (!(r.mask & (1u << kind))) {
       keep.push_back(r);
       continue;
     }
@@ -826,8 +841,13 @@ int sd_profile_read(sd_ctx* ctx, int kind, int64_t* count, double* ms, double* b
       t += e;
       by += r.bytes;
     }
-    hipEventDestroy(r.a);
-    hipEventDestroy(r.b);
+    r.mask &= ~(1u << kind);
+    if (r.mask) {
+      keep.push_back(r);
+    } else {
+      hipEventDestroy(r.a);
+      hipEventDestroy(r.b);
+    }
   }
   ctx->recs.swap(keep);
   if (count) *count = n;

@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -192,12 +193,22 @@ enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_PA
 
 hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s);
 hipError_t launch_rmsnorm(int dtype, const NormParams& p, hipStream_t s);
+// Kernel launch; with a start event the launch carries (start, stop) events
+// that the dispatch itself timestamps (kernel begin / end), as profilers do.
+template <typename K, typename... A>
+inline void launch_k(K kern, dim3 grid, dim3 block, uint32_t shm, hipStream_t s, hipEvent_t e0, hipEvent_t e1,
+                     A... args) {
+  if (e0) hipExtLaunchKernelGGL(kern, grid, block, shm, s, e0, e1, 0, args...);
+  else hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
+}
+
 int gemm_max_waves(int mt, int nt);   // waves per workgroup the (mt, nt) tile allows
 hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
-                       const GemmParams& p, hipStream_t s);
+                       const GemmParams& p, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // tab[pos * half + i] = (cos, sin) of pos * theta^(-i/half), pos < n_pos, i < half
 hipError_t launch_rope_table(float2* tab, int n_pos, int half, double theta, hipStream_t s);
-hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s);
+hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEvent_t e0 = nullptr,
+                            hipEvent_t e1 = nullptr);
 hipError_t launch_softmax(const SoftmaxParams& p, hipStream_t s);
 hipError_t launch_draft_sample(const DraftSampleParams& p, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
