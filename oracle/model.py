@@ -43,14 +43,35 @@ def round_bf16(x) -> np.ndarray:
     return a
 
 
+def _decode_f64(a: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "bf16":
+        return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    return np.asarray(a, dtype=np.float32).astype(np.float64)
+
+
 def weights_to_f64(w: Dict[str, np.ndarray], dtype: str) -> Dict[str, np.ndarray]:
-    """Decode stored weights (bf16 bit patterns or float32) into float64."""
+    """Decode stored weights (bf16 bit patterns or float32) into float64
+    (exact; large tensors are decoded in row chunks on a thread pool)."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
     out = {}
+    jobs = []
     for k, a in w.items():
-        if dtype == "bf16":
-            out[k] = (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+        if a.ndim == 2 and a.size >= (1 << 22):
+            o = np.empty(a.shape, dtype=np.float64)
+            out[k] = o
+            step = max(1, (1 << 21) // a.shape[1])
+            jobs += [(a, o, r, min(r + step, a.shape[0])) for r in range(0, a.shape[0], step)]
         else:
-            out[k] = np.asarray(a, dtype=np.float32).astype(np.float64)
+            out[k] = _decode_f64(a, dtype)
+
+    def run(job):
+        a, o, r0, r1 = job
+        o[r0:r1] = _decode_f64(a[r0:r1], dtype)
+
+    if jobs:
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(run, jobs))
     return out
 
 
