@@ -83,9 +83,9 @@ typedef struct {
  * sd_init copies them.
  *   wqkv  [(n_heads + 2 n_kv_heads) head_dim, d_model]: query rows (head
  *         major), then key rows, then value rows.  The rows of each query
- *         and key head are in rotary pair order: for b < head_dim / 32,
- *         rows 32b..32b+15 of the head are its dims 16b..16b+15 and rows
- *         32b+16..32b+31 its dims head_dim/2+16b..+15 (the two halves that
+ *         and key head are in rotary pair order: for b < head_dim / 16,
+ *         rows 16b..16b+7 of the head are its dims 8b..8b+7 and rows
+ *         16b+8..16b+15 its dims head_dim/2+8b..+7 (the two halves that
  *         the rotary embedding rotates together); value rows are in plain
  *         order.
  *   wo    [d_model, n_heads head_dim]

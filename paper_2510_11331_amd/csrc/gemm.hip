@@ -27,8 +27,10 @@
 //     cross-workgroup synchronisation, deterministic);
 //   * epilogues: store fp32, add into the fp32 residual stream, SwiGLU over
 //     interleaved gate/up rows (written in the model dtype), or, for the QKV
-//     projection, the rotary embedding of q and k over pair-ordered rows
-//     with q stored in fp32 and k, v appended to the paged KV cache.
+//     projection, the rotary embedding of q and k (rows in rotary pair
+//     order: the two halves of a pair sit 8 columns apart in one tile and
+//     meet through a lane exchange) with q stored in fp32 and k, v appended
+//     to the paged KV cache.
 #include "sd_internal.h"
 
 #include <algorithm>
@@ -179,7 +181,6 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     for (int v = 0; v < 4; ++v) {
       if ((4 * i + v) % KW != wave) continue;
       const int m = m0 + 16 * i + 4 * g + v;
-      if (m >= p.M) continue;
       float o[NT];
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
@@ -187,6 +188,14 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
         for (int w = 1; w < nslot; ++w) t += red[w][(i * NT + j) * 4 + v][lane];
         o[j] = t;
       }
+      // QKV: the rotary partner of column r16 is column r16 ^ 8 of the same
+      // tile (exchanged while the whole wave is still converged)
+      float pr[EPI == EPI_QKV ? NT : 1];
+      if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j) pr[j] = __shfl_xor(o[j], 8);
+      }
+      if (m >= p.M) continue;
       if constexpr (EPI == EPI_QKV) {
         const RopeParams& rp = p.rope;
         const int pos = rp.row_pos[m];
@@ -197,29 +206,22 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
         T* kv = (T*)rp.kv;
         const size_t kblk = (size_t)max(blk, 0) * 2 * rp.KV * 16 * hd, vblk = kblk + (size_t)rp.KV * 16 * hd;
 #pragma unroll
-        for (int j = 0; j < NT; j += 2) {
-          const int c0 = n0 + 16 * j;           // pair of 16-row tiles, 32-aligned
+        for (int j = 0; j < NT; ++j) {
+          const int c0 = n0 + 16 * j;           // first column of the tile
           if (c0 < Nqk) {
-            // tiles j, j+1 hold dims 16b + r16 and hd/2 + 16b + r16 of head h
-            const int h = c0 / hd, d1 = 16 * ((c0 % hd) / 32) + r16, d2 = d1 + half;
-            const float2 cs = rp.tab[(size_t)pos * half + d1];
-            const float a = o[j], b = o[j + 1];
-            const float o1 = a * cs.x - b * cs.y, o2 = a * cs.y + b * cs.x;
-            if (h < rp.H) {
-              float* q = rp.q + (size_t)m * Nq + (size_t)h * hd;
-              q[d1] = o1;
-              q[d2] = o2;
-            } else if (blk >= 0) {
-              const size_t kb = kblk + (size_t)(h - rp.H) * 16 * hd;
-              Store<T>::store(kv, kb + kv_key_off<T>(off, d1, hd), o1);
-              Store<T>::store(kv, kb + kv_key_off<T>(off, d2, hd), o2);
-            }
+            // rotary pair order: column r16 < 8 of the tile is dim 8b + r16 of
+            // head h, column r16 + 8 its partner dim hd/2 + 8b + r16
+            const int h = c0 / hd, f = 8 * ((c0 % hd) / 16) + (r16 & 7);
+            const int d = r16 < 8 ? f : f + half;
+            const float2 cs = rp.tab[(size_t)pos * half + f];
+            const float a = r16 < 8 ? o[j] : pr[j], b = r16 < 8 ? pr[j] : o[j];
+            const float y = r16 < 8 ? a * cs.x - b * cs.y : a * cs.y + b * cs.x;
+            if (h < rp.H) rp.q[(size_t)m * Nq + (size_t)h * hd + d] = y;
+            else if (blk >= 0)
+              Store<T>::store(kv, kblk + (size_t)(h - rp.H) * 16 * hd + kv_key_off<T>(off, d, hd), y);
           } else if (blk >= 0) {
-#pragma unroll
-            for (int jj = j; jj < j + 2; ++jj) {
-              const int cv = c0 + 16 * (jj - j) + r16 - Nqk;
-              Store<T>::store(kv, vblk + (size_t)(cv / hd) * 16 * hd + (size_t)(cv % hd) * 16 + off, o[jj]);
-            }
+            const int cv = c0 + r16 - Nqk;
+            Store<T>::store(kv, vblk + (size_t)(cv / hd) * 16 * hd + (size_t)(cv % hd) * 16 + off, o[j]);
           }
         }
       } else if constexpr (EPI == EPI_SWIGLU) {
@@ -297,9 +299,13 @@ static hipError_t launch_nt(int nt, int mt, dim3 grid, int threads, const GemmPa
                             hipEvent_t e1) {
   switch (nt) {
     case 1:
-      if constexpr (EPI != EPI_SWIGLU && EPI != EPI_QKV) return launch_mt<T, EPI, 1, GEMM_U>(mt, grid, threads, p, s, e0, e1);
+      if constexpr (EPI != EPI_SWIGLU) return launch_mt<T, EPI, 1, GEMM_U>(mt, grid, threads, p, s, e0, e1);
       return hipErrorInvalidValue;
     case 2: return launch_mt<T, EPI, 2, GEMM_U>(mt, grid, threads, p, s, e0, e1);
+    case 3:
+      // 48-column tiles: only the QKV projection uses them (one tile per CU at 7B)
+      if constexpr (EPI == EPI_QKV) return launch_mt<T, EPI, 3, GEMM_U>(mt, grid, threads, p, s, e0, e1);
+      return hipErrorInvalidValue;
     case 4: return launch_mt<T, EPI, 4, GEMM_U>(mt, grid, threads, p, s, e0, e1);
     default: return hipErrorInvalidValue;
   }
@@ -315,7 +321,7 @@ hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, i
     return hipErrorInvalidValue;
   dim3 grid(grid_x, ksplit, grid_z);
   const int threads = 64 * kw;
-  if (epi == EPI_QKV && (p.rope.hd % 32 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd)) return hipErrorInvalidValue;
+  if (epi == EPI_QKV && (p.rope.hd % 16 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd)) return hipErrorInvalidValue;
   if (dtype == 0) {
     if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, p, s, e0, e1);
     if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, p, s, e0, e1);

@@ -288,9 +288,11 @@ struct GemmPlan {
 // it.  Chosen from sweeps on MI355X with packed operands at M = 40 and M = 8
 // (7B-shape verify and draft passes, weights streamed from HBM):
 //   * SwiGLU gate/up: 32-column tiles, 8 waves;
-//   * QKV and LM head: 64-column tiles with 6 waves when that leaves ~170+
-//     workgroups, else 32-column tiles with 8 waves (QKV needs an even
-//     number of tiles for the rotary pairs);
+//   * QKV: 16-column tiles at M <= 16; else 48-column tiles (at 7B, 256
+//     workgroups = one per CU: 23 us against 25 us for 64-column tiles on
+//     192 workgroups);
+//   * LM head (and QKV where 48 does not divide N): 64-column tiles with 6
+//     waves when that leaves ~170+ workgroups, else 32-column tiles;
 //   * residual projections (O, down), M <= 64 with an RMSNorm after them
 //     (split_ok): few column tiles, so K is split over workgroups until
 //     there are ~256 of them (32-column tiles at M > 16); the partial sums
@@ -307,6 +309,10 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
   const int groups = (int)(K * esz / 64) / GEMM_U;   // k-step groups of one wave step
   if (epi == EPI_SWIGLU) {
     g.nt = 2;
+  } else if (epi == EPI_QKV && g.mt == 1) {
+    g.nt = 1;                                         // draft-sized M: most workgroups
+  } else if (epi == EPI_QKV && g.mt <= 3 && N % 48 == 0 && N / 48 <= 320) {
+    g.nt = 3;                                         // up to ~one workgroup per CU
   } else if (epi == EPI_RESID && split_ok && g.gz == 1) {
     g.nt = (g.mt >= 2 && N % 32 == 0) ? 2 : 1;
     const int gx = N / (16 * g.nt);
@@ -315,7 +321,7 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
   } else if (g.mt <= 3 && N % 64 == 0 && N / 64 >= 170) {
     g.nt = 4;                                         // 64-row blocks take at most 32 columns
     g.kw = 6;
-  } else if (N % 32 == 0 && (N / 32 >= 170 || epi == EPI_QKV)) {
+  } else if (N % 32 == 0 && N / 32 >= 170) {
     g.nt = 2;
   } else {
     g.nt = 1;

@@ -41,10 +41,10 @@ def interleave_gate_up(gate: np.ndarray, up: np.ndarray) -> np.ndarray:
 
 def rotary_pair_order(w: np.ndarray, head_dim: int) -> np.ndarray:
     """[heads * hd, d] query or key rows -> the same rows with each head in
-    rotary pair order: for b < hd/32, rows 32b..32b+15 are dims 16b..16b+15
-    and rows 32b+16..32b+31 are dims hd/2+16b..hd/2+16b+15."""
+    rotary pair order: for b < hd/16, rows 16b..16b+7 are dims 8b..8b+7 and
+    rows 16b+8..16b+15 are dims hd/2+8b..hd/2+8b+7."""
     n, d = w.shape
-    h = w.reshape(n // head_dim, 2, head_dim // 32, 16, d)      # [head, half, b, 16, d]
+    h = w.reshape(n // head_dim, 2, head_dim // 16, 8, d)       # [head, half, b, 8, d]
     return np.ascontiguousarray(h.transpose(0, 2, 1, 3, 4)).reshape(n, d)
 
 
