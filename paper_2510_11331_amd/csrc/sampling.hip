@@ -15,18 +15,17 @@
 //   residual w_j = max(0, p_j - q_j) with a correctly rounded float32 subtract.
 //
 // A row (up to 32768 entries) is held in registers by one 1024-thread
-// workgroup: for sampling each thread owns 32 consecutive entries (so the
-// prefix sum in index order is one block scan of per-thread totals); the
-// plain softmax uses a strided float4 layout for coalescing.  All loads of a
-// row are issued before any is used.
+// workgroup in a strided float4 layout (coalesced loads and stores); the
+// prefix sums of a draw are taken in index order from wave scans.  All loads
+// of a row are issued before any is used.
 #include "sd_internal.h"
 
 namespace sd {
 
 constexpr int RT = 1024;          // threads of a row kernel
 constexpr int NW = RT / 64;       // waves
-constexpr int SEG = 32;           // consecutive entries per thread in sampling kernels
-constexpr int SV = SEG / 4;       // float4 per thread in the strided layout (V <= RT * 4 * SV)
+constexpr int SV = 8;             // float4 per thread in the strided layout (V <= RT * 4 * SV)
+static_assert(SV * NW % 64 == 0, "draft sampling scans SV * NW totals with one wave");
 
 __device__ __forceinline__ float wmax(float v) {
 #pragma unroll
@@ -79,71 +78,16 @@ __device__ int block_argmax(float v, int i, float* redv, int* redi) {
   return bi;
 }
 
-// exclusive prefix of per-thread uint64 values in thread order; *total = sum
-__device__ uint64_t block_excl_scan(uint64_t v, uint64_t* red, uint64_t* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  unsigned long long x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const unsigned long long y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  __syncthreads();
-  if (lane == 63) red[wave] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint64_t a = 0;
-    for (int w = 0; w < NW; ++w) { const uint64_t t = red[w]; red[w] = a; a += t; }
-    red[NW] = a;
-  }
-  __syncthreads();
-  *total = red[NW];
-  return red[wave] + x - v;
-}
-
+// floor(w 2^40) for 0 <= w < 2^23, exactly: x = w 2^40 is exact in float32;
+// hi = floor(x / 2^32) and lo = x - hi 2^32 are exact too (when hi > 0,
+// x >= 2^32 has an ulp of at least 2^9, so lo is a representable multiple of
+// it below 2^32), and the float -> uint32 conversion of lo truncates = floors.
 __device__ __forceinline__ uint64_t fixed40(float w) {
-  // w >= 0; w * 2^40 is exact in float32, truncation is the floor
-  return w > 0.f ? (uint64_t)(w * 1099511627776.0f) : 0ull;
-}
-
-// thread-contiguous segment of a row: entries [SEG*t, SEG*t + SEG) (0 beyond V)
-__device__ __forceinline__ void load_seg(const float* row, int V, float (&v)[SEG]) {
-  const int j0 = threadIdx.x * SEG;
-  if (j0 + SEG <= V && (V & 3) == 0) {
-#pragma unroll
-    for (int k = 0; k < SV; ++k) {
-      const float4 x = *(const float4*)(row + j0 + 4 * k);
-      v[4 * k] = x.x; v[4 * k + 1] = x.y; v[4 * k + 2] = x.z; v[4 * k + 3] = x.w;
-    }
-  } else {
-#pragma unroll
-    for (int k = 0; k < SEG; ++k) v[k] = j0 + k < V ? row[j0 + k] : 0.f;
-  }
-}
-
-// Integer inverse-CDF draw over the weights w (this thread's segment);
-// returns -1 if S == 0.
-__device__ int seg_sample(const float (&w)[SEG], uint32_t r, uint64_t* red, int* result) {
-  uint64_t local = 0;
-#pragma unroll
-  for (int k = 0; k < SEG; ++k) local += fixed40(w[k]);
-  if (threadIdx.x == 0) *result = -1;
-  uint64_t S;
-  const uint64_t lo = block_excl_scan(local, red, &S);
-  if (S == 0) return -1;
-  const uint64_t T = (S >> 32) * (uint64_t)r + (((S & 0xffffffffull) * (uint64_t)r) >> 32);
-  if (T >= lo && T < lo + local) {                // this thread's segment holds the draw
-    int hit = SEG - 1;
-    uint64_t pre = lo;
-#pragma unroll
-    for (int k = 0; k < SEG; ++k) {                // smallest k with lo + prefix_k > T
-      pre += fixed40(w[k]);
-      if (pre > T) { hit = k; break; }
-    }
-    *result = threadIdx.x * SEG + hit;
-  }
-  __syncthreads();
-  return *result;
+  if (!(w > 0.f)) return 0ull;
+  const float x = w * 1099511627776.0f;
+  const float hi = floorf(x * 2.3283064365386963e-10f);
+  const float lo = x - hi * 4294967296.0f;
+  return ((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo;
 }
 
 __global__ __launch_bounds__(RT) void softmax_kernel(SoftmaxParams p) {
@@ -187,73 +131,156 @@ __global__ __launch_bounds__(RT) void softmax_kernel(SoftmaxParams p) {
   }
 }
 
-__global__ __launch_bounds__(RT) void draft_sample_kernel(DraftSampleParams p) {
-  __shared__ float red[NW];
-  __shared__ int redi[NW];
-  __shared__ uint64_t redu[NW + 1];
-  __shared__ int result;
-  const int b = blockIdx.x;
-  const float* z = p.z + (size_t)b * p.V;
-  float* q = p.q + ((size_t)b * p.gamma + p.i) * p.V;
-  const int j0 = threadIdx.x * SEG;
-  float v[SEG];
-  load_seg(z, p.V, v);
-  int tok;
-  if (p.greedy) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-#pragma unroll
-    for (int k = 0; k < SEG; ++k)
-      if (j0 + k < p.V && v[k] > bv) { bv = v[k]; bi = j0 + k; }
-    tok = block_argmax(bv, bi, red, redi);
-    if (tok == 0x7fffffff) tok = 0;
-#pragma unroll
-    for (int k = 0; k < SEG; ++k)
-      if (j0 + k < p.V) q[j0 + k] = v[k];
-  } else {
-    float m = -INFINITY;
-#pragma unroll
-    for (int k = 0; k < SEG; ++k) {
-      v[k] *= p.inv_tau;
-      if (j0 + k < p.V) m = fmaxf(m, v[k]);
-    }
-    m = block_max(m, red);
-    float s = 0.f;
-#pragma unroll
-    for (int k = 0; k < SEG; ++k) {
-      v[k] = j0 + k < p.V ? expf(v[k] - m) : 0.f;
-      s += v[k];
-    }
-    s = block_sum(s, red);
-#pragma unroll
-    for (int k = 0; k < SEG; ++k) {
-      v[k] = v[k] / s;
-      if (j0 + k < p.V) q[j0 + k] = v[k];
-    }
-    const uint32_t r = p.u[(size_t)b * (2 * p.gamma + 1) + p.i];
-    tok = seg_sample(v, r, redu, &result);
-    if (tok < 0) tok = 0;                       // no integer mass: impossible for a softmax row
-  }
-  if (threadIdx.x == 0) p.draft_tok[b * p.gamma + p.i] = tok;
+// x moved by a DPP pattern, 0 where the source lane is out of the row or
+// the destination row is masked off
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, ROWS, 0xf, true);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, ROWS, 0xf, true);
+  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
 }
 
-__device__ int row_argmax(const float* row, int V, float* red, int* redi) {
-  float v[SEG];
-  load_seg(row, V, v);
-  const int j0 = threadIdx.x * SEG;
+// inclusive scan of uint64 values over the 64 lanes of a wave (register-file
+// moves: shifts by 1, 2, 4, 8 inside each 16-lane row, then the last lane of
+// row 0 / 2 broadcast into rows 1 / 3 and of row 1 into rows 2, 3)
+__device__ __forceinline__ uint64_t wave_incl_scan(uint64_t x) {
+  x += dpp_u64<0x111, 0xf>(x);    // row_shr:1
+  x += dpp_u64<0x112, 0xf>(x);    // row_shr:2
+  x += dpp_u64<0x114, 0xf>(x);    // row_shr:4
+  x += dpp_u64<0x118, 0xf>(x);    // row_shr:8
+  x += dpp_u64<0x142, 0xa>(x);    // row_bcast:15 into rows 1, 3
+  x += dpp_u64<0x143, 0xc>(x);    // row_bcast:31 into rows 2, 3
+  return x;
+}
+
+// Strided float4 layout of a row (coalesced): thread t holds entries
+// 4 (t + RT k) .. +3 for k < SV; entries past V read as `fill`.  Index order
+// is k-major, then thread, then the 4 entries.
+__device__ __forceinline__ void load_strided(const float* row, int V, float4 (&x)[SV], float fill) {
+  const int V4 = V >> 2;
+#pragma unroll
+  for (int k = 0; k < SV; ++k) {
+    const int i = threadIdx.x + RT * k;
+    x[k] = i < V4 ? ((const float4*)row)[i] : make_float4(fill, fill, fill, fill);
+  }
+}
+
+// Arg-max of a strided row, lowest index on ties (entries are visited in
+// increasing index, so a thread's first strict maximum is its lowest).
+__device__ int strided_argmax(const float4 (&x)[SV], float* red, int* redi) {
   float bv = -INFINITY;
   int bi = 0x7fffffff;
 #pragma unroll
-  for (int k = 0; k < SEG; ++k)
-    if (j0 + k < V && v[k] > bv) { bv = v[k]; bi = j0 + k; }
+  for (int k = 0; k < SV; ++k) {
+    const int j = 4 * (threadIdx.x + RT * k);
+    if (x[k].x > bv) { bv = x[k].x; bi = j; }
+    if (x[k].y > bv) { bv = x[k].y; bi = j + 1; }
+    if (x[k].z > bv) { bv = x[k].z; bi = j + 2; }
+    if (x[k].w > bv) { bv = x[k].w; bi = j + 3; }
+  }
   const int r = block_argmax(bv, bi, red, redi);
   return r == 0x7fffffff ? 0 : r;
+}
+
+// Integer inverse-CDF draw over strided weights w (>= 0, zero past V) with
+// uniform r; -1 if S = 0.  The prefix of W_j = floor(w_j 2^40) in index order
+// comes from a wave scan of the per-thread sums of each chunk k and one scan
+// over the (k, wave) totals.  Called by every thread of the workgroup.
+__device__ int strided_sample(const float4 (&w)[SV], uint32_t r, uint64_t* pre, uint64_t* total, int* result) {
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  __syncthreads();                              // a previous draw's result has been read
+  uint64_t L[SV], excl[SV];
+#pragma unroll
+  for (int k = 0; k < SV; ++k) {
+    L[k] = fixed40(w[k].x) + fixed40(w[k].y) + fixed40(w[k].z) + fixed40(w[k].w);
+    const uint64_t inc = wave_incl_scan(L[k]);
+    excl[k] = inc - L[k];
+    if (lane == 63) pre[k * NW + wave] = inc;
+  }
+  if (t == 0) *result = -1;
+  __syncthreads();
+  if (wave == 0) {
+    // exclusive prefix of the SV * NW totals in (k, wave) order
+    constexpr int PER = SV * NW / 64;
+    uint64_t a[PER], s = 0;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) { a[e] = pre[PER * lane + e]; s += a[e]; }
+    const uint64_t inc = wave_incl_scan(s);
+    uint64_t run = inc - s;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) { pre[PER * lane + e] = run; run += a[e]; }
+    if (lane == 63) *total = inc;
+  }
+  __syncthreads();
+  const uint64_t S = *total;
+  const uint64_t T = (S >> 32) * (uint64_t)r + (((S & 0xffffffffull) * (uint64_t)r) >> 32);
+#pragma unroll
+  for (int k = 0; k < SV; ++k) {
+    const uint64_t lo = pre[k * NW + wave] + excl[k];
+    if (S > 0 && T >= lo && T < lo + L[k]) {      // this thread's 4 entries of chunk k hold the draw
+      const float v[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
+      uint64_t c = lo;
+      int hit = 3;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        c += fixed40(v[e]);
+        if (c > T) { hit = e; break; }
+      }
+      *result = 4 * (t + RT * k) + hit;
+    }
+  }
+  __syncthreads();
+  return *result;
+}
+
+__global__ __launch_bounds__(RT) void draft_sample_kernel(DraftSampleParams p) {
+  __shared__ float red[NW];
+  __shared__ int redi[NW];
+  __shared__ uint64_t pre[SV * NW];
+  __shared__ uint64_t total;
+  __shared__ int result;
+  const int b = blockIdx.x, t = threadIdx.x;
+  float4* q = (float4*)(p.q + ((size_t)b * p.gamma + p.i) * p.V);
+  const int V4 = p.V >> 2;
+  float4 x[SV];
+  load_strided(p.z + (size_t)b * p.V, p.V, x, -INFINITY);
+  int tok;
+  if (p.greedy) {
+#pragma unroll
+    for (int k = 0; k < SV; ++k)
+      if (t + RT * k < V4) q[t + RT * k] = x[k];
+    tok = strided_argmax(x, red, redi);
+  } else {
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < SV; ++k) {
+      x[k].x *= p.inv_tau; x[k].y *= p.inv_tau; x[k].z *= p.inv_tau; x[k].w *= p.inv_tau;
+      m = fmaxf(m, fmaxf(fmaxf(x[k].x, x[k].y), fmaxf(x[k].z, x[k].w)));
+    }
+    m = block_max(m, red);
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < SV; ++k) {
+      x[k].x = expf(x[k].x - m); x[k].y = expf(x[k].y - m); x[k].z = expf(x[k].z - m); x[k].w = expf(x[k].w - m);
+      sum += (x[k].x + x[k].y) + (x[k].z + x[k].w);
+    }
+    const float inv = 1.0f / block_sum(sum, red);
+#pragma unroll
+    for (int k = 0; k < SV; ++k) {
+      x[k].x *= inv; x[k].y *= inv; x[k].z *= inv; x[k].w *= inv;
+      if (t + RT * k < V4) q[t + RT * k] = x[k];
+    }
+    tok = strided_sample(x, p.u[(size_t)b * (2 * p.gamma + 1) + p.i], pre, &total, &result);
+    if (tok < 0) tok = 0;                       // no integer mass: impossible for a softmax row
+  }
+  if (t == 0) p.draft_tok[b * p.gamma + p.i] = tok;
 }
 
 __global__ __launch_bounds__(RT) void accept_kernel(AcceptParams p) {
   __shared__ float red[NW];
   __shared__ int redi[NW];
-  __shared__ uint64_t redu[NW + 1];
+  __shared__ uint64_t pre[SV * NW];
+  __shared__ uint64_t total;
   __shared__ int result, s_a;
   const int b = blockIdx.x, g = p.gamma, V = p.V;
   const int32_t* dt = p.draft_tok + (size_t)b * g;
@@ -261,12 +288,17 @@ __global__ __launch_bounds__(RT) void accept_kernel(AcceptParams p) {
   const float* pp = p.p + (size_t)b * (g + 1) * V;
   const uint32_t* u = p.u + (size_t)b * (2 * g + 1);
   int a = g, y = 0;
+  float4 w[SV];
   if (p.greedy) {
     for (int i = 0; i < g; ++i) {
-      const int am = row_argmax(pp + (size_t)i * V, V, red, redi);
+      load_strided(pp + (size_t)i * V, V, w, -INFINITY);
+      const int am = strided_argmax(w, red, redi);
       if (dt[i] != am) { a = i; y = am; break; }
     }
-    if (a == g) y = row_argmax(pp + (size_t)g * V, V, red, redi);
+    if (a == g) {
+      load_strided(pp + (size_t)g * V, V, w, -INFINITY);
+      y = strided_argmax(w, red, redi);
+    }
   } else {
     if (threadIdx.x == 0) {
       int aa = g;
@@ -286,20 +318,27 @@ __global__ __launch_bounds__(RT) void accept_kernel(AcceptParams p) {
     __syncthreads();
     a = s_a;
     const uint32_t r = u[2 * g];
-    float w[SEG];
-    load_seg(pp + (size_t)a * V, V, w);
+    load_strided(pp + (size_t)a * V, V, w, 0.f);
     if (a < g) {
-      float res[SEG];
-      load_seg(q + (size_t)a * V, V, res);
+      const float* qa = q + (size_t)a * V;
+      const int V4 = V >> 2;
 #pragma unroll
-      for (int k = 0; k < SEG; ++k) {
-        const float d = __fsub_rn(w[k], res[k]);
-        res[k] = d > 0.f ? d : 0.f;
+      for (int k = 0; k < SV; ++k) {
+        // max(0, p - q) with a correctly rounded subtraction, in place
+        const int i = threadIdx.x + RT * k;
+        const float4 qv = i < V4 ? ((const float4*)qa)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+        w[k].x = fmaxf(__fsub_rn(w[k].x, qv.x), 0.f);
+        w[k].y = fmaxf(__fsub_rn(w[k].y, qv.y), 0.f);
+        w[k].z = fmaxf(__fsub_rn(w[k].z, qv.z), 0.f);
+        w[k].w = fmaxf(__fsub_rn(w[k].w, qv.w), 0.f);
       }
-      y = seg_sample(res, r, redu, &result);
-      if (y < 0) y = seg_sample(w, r, redu, &result);      // residual without integer mass
+      y = strided_sample(w, r, pre, &total, &result);
+      if (y < 0) {                               // residual without integer mass: draw from p
+        load_strided(pp + (size_t)a * V, V, w, 0.f);
+        y = strided_sample(w, r, pre, &total, &result);
+      }
     } else {
-      y = seg_sample(w, r, redu, &result);
+      y = strided_sample(w, r, pre, &total, &result);
     }
     if (y < 0) y = 0;
   }
@@ -331,19 +370,19 @@ __global__ void commit_kernel(CommitParams p) {
 
 hipError_t launch_softmax(const SoftmaxParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
-  if (p.V > RT * SEG || (p.V & 3)) return hipErrorInvalidValue;
+  if (p.V > RT * 4 * SV || (p.V & 3)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(softmax_kernel, dim3(p.M), dim3(RT), 0, s, p);
   return hipGetLastError();
 }
 hipError_t launch_draft_sample(const DraftSampleParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  if (p.V > RT * SEG) return hipErrorInvalidValue;
+  if (p.V > RT * 4 * SV) return hipErrorInvalidValue;
   hipLaunchKernelGGL(draft_sample_kernel, dim3(p.B), dim3(RT), 0, s, p);
   return hipGetLastError();
 }
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  if (p.V > RT * SEG) return hipErrorInvalidValue;
+  if (p.V > RT * 4 * SV) return hipErrorInvalidValue;
   hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(RT), 0, s, p);
   return hipGetLastError();
 }

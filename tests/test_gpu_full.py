@@ -21,7 +21,7 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import model as om
+from oracle import model as om, sampling as osp
 from sdcase import say, make_engine, run_gpu_steps
 
 pytestmark = pytest.mark.gpu
@@ -74,6 +74,12 @@ def _check(tshape, dshape, tseed, dseed, B, gamma, prompt_len, sample_tasks):
         say("task", k, "worst target logit err", worst_p, "worst draft err", worst_q)
     assert worst_p < 2e-2, worst_p
     assert worst_q < 2e-2, worst_q
+    # every draft token is the integer inverse-CDF draw from the GPU's own q
+    # with that slot's uniform (bit-exact at the full vocabulary)
+    ut = synth.uniform_table(42, slots, 1, gamma)[0]
+    for k in range(B):
+        for j in range(gamma):
+            assert int(draft_tok[k, j]) == osp.sample_weights(q[k, j], int(ut[k, j])), (k, j)
     # invariants of the step at this size
     assert ((acc >= 0) & (acc <= gamma)).all()
     for k in range(B):
