@@ -3,12 +3,15 @@
 // epilogue; eq. d_atte / f21 attend with softmax(q K^T / sqrt(d0)) V), and
 // the rotary (cos, sin) table that epilogue reads.
 //
-// Paged layout of one layer's pool, per 16-token block and kv head: K in the
-// layout of the S = K Q^T matrix instruction for bf16 (kv_key_off: every
-// wave load of a key k-step is a contiguous 1 KB) or as [16 tokens][hd] for
-// fp32, V transposed as [hd][16 tokens] (so the P*V operand of a matrix
-// instruction is 4 consecutive tokens of one dimension); a slot's block
-// table maps position / 16 to a block.
+// Paged layout of one layer's pool: head-major tiles [kv head][block][K|V]
+// (kv_tile_off), so that the blocks of one task and head, allocated in
+// order, are one contiguous run; K in the layout of the S = K Q^T matrix
+// instruction for bf16 (kv_key_off: every wave load of a key k-step is a
+// contiguous 1 KB) or as [16 tokens][hd] for fp32; V transposed so that the
+// P*V operand of a matrix instruction is 4 consecutive tokens of one
+// dimension (kv_val_off: for bf16 two such quads per 16-byte unit, 1 KB per
+// wave load; [hd][16 tokens] for fp32); a slot's block table maps position /
+// 16 to a block.
 //
 // Attention work item = (row block, kv head, key split).  A row block is a
 // run of consecutive rows of one task (the gamma+1 verify rows of a task, its
@@ -17,8 +20,7 @@
 // every K/V tile.  Query i only sees keys at positions <= its own.  Each work
 // item keeps an online softmax (running max, running sum, rescaled output);
 // when the keys are split, partial (max, sum, output) triples go to a
-// workspace and the last-arriving workgroup of the (row block, kv head)
-// merges them in split order.
+// workspace and a second kernel merges them in split order.
 //
 // bf16 models: S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_16x16x32_bf16,
 // 16 query vectors per wave, keys streamed from the cache straight into
@@ -84,7 +86,6 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
   constexpr int EPU = KvT<T>::EPU;
   constexpr int NQG = 256 / HD;            // query groups in the P*V phase
   constexpr int QPT = ATTN_QMAX / NQG;     // query vectors per thread in P*V
-  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rbk = blockIdx.x;
@@ -153,11 +154,11 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
       for (int t = 0; t < EPU; ++t) vv[t] = T(0);
       if (kp < k_end) {
         const int blk = bt[kp / 16];
-        const size_t base = (((size_t)blk * 2) * p.KV + kvh) * 16 * HD + (size_t)(kp % 16) * HD + e;
-        const size_t vtb = (((size_t)blk * 2 + 1) * p.KV + kvh) * 16 * HD + (kp % 16);
+        const size_t base = kv_tile_off(kvh, blk, 0, p.nblk, HD) + (size_t)(kp % 16) * HD + e;
+        const size_t vtb = kv_tile_off(kvh, blk, 1, p.nblk, HD);
         kk = *(const uint4*)(kv + base);
 #pragma unroll
-        for (int t = 0; t < EPU; ++t) vv[t] = kv[vtb + (size_t)(e + t) * 16];   // V stored [hd][16]
+        for (int t = 0; t < EPU; ++t) vv[t] = kv[vtb + kv_val_off<T>(kp % 16, e + t, HD)];
       }
       uint32_t* kd = (uint32_t*)(Ks + j * KST + e);   // KST*esz is a multiple of 4
       kd[0] = kk.x; kd[1] = kk.y; kd[2] = kk.z; kd[3] = kk.w;
@@ -220,6 +221,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
     return;
   }
 
+  // key split: partial (output, max, sum) for attn_merge_kernel
   const size_t item = (size_t)rbk * p.splits;
 #pragma unroll
   for (int k = 0; k < QPT; ++k) {
@@ -230,31 +232,6 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
     p.part_ml[((item + split) * qmax + qi) * 2 + 0] = Ms[qi];
     p.part_ml[((item + split) * qmax + qi) * 2 + 1] = Ls[qi];
   }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = atomicAdd(&p.counters[rbk], 1) == p.splits - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-#pragma unroll
-  for (int k = 0; k < QPT; ++k) {
-    const int qi = qg + NQG * k;
-    if (qi >= Qn) continue;
-    float M = -INFINITY;
-    for (int sp = 0; sp < p.splits; ++sp) M = fmaxf(M, p.part_ml[((item + sp) * qmax + qi) * 2]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
-      for (int sp = 0; sp < p.splits; ++sp) {
-        const float m = p.part_ml[((item + sp) * qmax + qi) * 2];
-        if (m == -INFINITY) continue;
-        const float w = expf(m - M);
-        L += p.part_ml[((item + sp) * qmax + qi) * 2 + 1] * w;
-        O += p.part_o[((item + sp) * qmax + qi) * HD + dd] * w;
-      }
-    }
-    emit(qi, L > 0.f ? O / L : 0.f);
-  }
-  if (tid == 0) p.counters[rbk] = 0;
 }
 
 // bf16 hi + lo pair of 8 floats, packed as two bf16x8 operands
@@ -287,7 +264,6 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
   constexpr int NSLOT = WAVES / 2;         // merge slots: half the waves hand over in the first round
   __shared__ float s_o[NSLOT][16][HD + 4];
   __shared__ float s_m[NSLOT][16], s_l[NSLOT][16];
-  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -341,12 +317,14 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
 
   const bf16_t* kv = (const bf16_t*)p.kv;
   const int32_t* bt = p.block_table + (size_t)slot * p.mbps;
-  const size_t blk_stride = (size_t)2 * p.KV * 16 * HD;
-  // key block in the matrix-instruction layout: k-step s is the 1 KB run at
+  // key tile in the matrix-instruction layout: k-step s is the 1 KB run at
   // unit 64 s, this lane's 16 bytes at unit 64 s + lane (token r16, dims
-  // g HD/4 + 8 s .. + 8)
-  const size_t koff = (size_t)kvh * 16 * HD + (size_t)lane * 8;
-  const size_t voff = (size_t)p.KV * 16 * HD + (size_t)kvh * 16 * HD + (size_t)r16 * 16 + 4 * g;
+  // g HD/4 + 8 s .. + 8); the V tile follows the K tile of the same block
+  const size_t koff = (size_t)lane * 8;
+  // V tile (kv_val_off): unit 4 r16 + g of 32-dim group dp holds tokens
+  // 4g..4g+3 of dims 32 dp + r16 and 32 dp + 16 + r16 (the 64 lanes read the
+  // group's 1 KB)
+  const size_t voff = (size_t)16 * HD + (size_t)(4 * r16 + g) * 8;
 
   // two register stages of one 32-key step: K rows (two blocks) and V^T quads
   u32x4 Kf[2][2][UPG];
@@ -357,7 +335,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
     for (int t = 0; t < 2; ++t) {
       const int bi = kb / 16 + t;
       const bool ok = bi < p.mbps && kb + 16 * t < k_end;
-      const bf16_t* base = kv + (size_t)(ok ? bt[bi] : 0) * blk_stride;
+      const bf16_t* base = kv + kv_tile_off(kvh, ok ? bt[bi] : 0, 0, p.nblk, HD);
 #pragma unroll
       for (int s = 0; s < UPG; ++s) Kf[S][t][s] = __builtin_nontemporal_load((const u32x4*)(base + koff + 512 * s));
       // keys at or past k_end were never written: their scores are masked, and
@@ -366,10 +344,12 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
       const uint32_t mx = nq >= 2 ? 0xffffffffu : (nq == 1 ? 0xffffu : 0u);
       const uint32_t my = nq >= 4 ? 0xffffffffu : (nq == 3 ? 0xffffu : 0u);
 #pragma unroll
-      for (int d = 0; d < DT; ++d) {
-        const u32x2 v = __builtin_nontemporal_load((const u32x2*)(base + voff + (size_t)d * 256));
-        Vf[S][t][d][0] = v.x & mx;
-        Vf[S][t][d][1] = v.y & my;
+      for (int dp = 0; dp < DT / 2; ++dp) {
+        const u32x4 v = __builtin_nontemporal_load((const u32x4*)(base + voff + (size_t)dp * 512));
+        Vf[S][t][2 * dp][0] = v.x & mx;
+        Vf[S][t][2 * dp][1] = v.y & my;
+        Vf[S][t][2 * dp + 1][0] = v.z & mx;
+        Vf[S][t][2 * dp + 1][1] = v.w & my;
       }
     }
   };
@@ -482,6 +462,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
     return;
   }
 
+  // key split: partial (output, max, sum) for attn_merge_kernel
   const size_t item = ((size_t)rbk * p.splits + split) * p.qmax + (owner ? qi : 0);
   if (owner) {
 #pragma unroll
@@ -493,38 +474,43 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
       p.part_ml[item * 2 + 1] = l_run;
     }
   }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = atomicAdd(&p.counters[rbk], 1) == p.splits - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  if (owner) {
-    const size_t base = (size_t)rbk * p.splits * p.qmax + qi;
+}
+
+// Merge of the key splits of every (row block, kv head) item, in split order:
+// O = sum_s o_s e^(m_s - M) / sum_s l_s e^(m_s - M), M = max_s m_s.  A second
+// kernel instead of a last-arriving workgroup: on MI355X a device-scope
+// release per workgroup costs more than a kernel boundary.
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+  const int rbk = blockIdx.x, rb = rbk / p.KV, kvh = rbk % p.KV;
+  int row0, nr;
+  if (p.rowblocks) {
+    row0 = p.rowblocks[2 * rb];
+    nr = p.rowblocks[2 * rb + 1];
+  } else {
+    row0 = rb * p.R;
+    nr = p.R;
+  }
+  const int G = p.H / p.KV, Qn = nr * G;
+  const size_t base = (size_t)rbk * p.splits * p.qmax;
+  for (int idx = threadIdx.x; idx < Qn * HD; idx += blockDim.x) {
+    const int qi = idx / HD, d = idx % HD;
     float M = -INFINITY;
-    for (int sp = 0; sp < p.splits; ++sp) M = fmaxf(M, p.part_ml[(base + (size_t)sp * p.qmax) * 2]);
-    float L = 0.f;
-    f32x4 O[DT];
-#pragma unroll
-    for (int d = 0; d < DT; ++d) O[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < p.splits; ++sp) M = fmaxf(M, p.part_ml[(base + (size_t)sp * p.qmax + qi) * 2]);
+    float L = 0.f, O = 0.f;
     if (M != -INFINITY) {
       for (int sp = 0; sp < p.splits; ++sp) {
-        const size_t it = base + (size_t)sp * p.qmax;
+        const size_t it = base + (size_t)sp * p.qmax + qi;
         const float m = p.part_ml[it * 2];
         if (m == -INFINITY) continue;
         const float w = expf(m - M);
         L += p.part_ml[it * 2 + 1] * w;
-#pragma unroll
-        for (int d = 0; d < DT; ++d)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) O[d][v] += p.part_o[it * HD + 16 * d + 4 * g + v] * w;
+        O += p.part_o[it * HD + d] * w;
       }
     }
-    const float inv = L > 0.f ? 1.0f / L : 0.f;
-#pragma unroll
-    for (int d = 0; d < DT; ++d) emit4(d, O[d][0] * inv, O[d][1] * inv, O[d][2] * inv, O[d][3] * inv);
+    const int row = row0 + qi / G, h = kvh * G + qi % G;
+    Store<T>::store((T*)p.out, Tile<T>::off(row, h * HD + d, p.H * HD), L > 0.f ? O / L : 0.f);
   }
-  if (tid == 0) p.counters[rbk] = 0;
 }
 
 hipError_t launch_rope_table(float2* tab, int n_pos, int half, double theta, hipStream_t s) {
@@ -545,7 +531,10 @@ static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s, hipEvent_t e
     if (e != hipSuccess) return e;
     attr_bytes = lds;
   }
-  launch_k(attention_kernel<T, HD>, dim3(p.nrb * p.KV, p.splits), dim3(256), (uint32_t)lds, s, e0, e1, p);
+  const bool split = p.splits > 1;
+  launch_k(attention_kernel<T, HD>, dim3(p.nrb * p.KV, p.splits), dim3(256), (uint32_t)lds, s, e0,
+           split ? nullptr : e1, p);
+  if (split) launch_k(attn_merge_kernel<T, HD>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
   return hipGetLastError();
 }
 
@@ -555,9 +544,17 @@ hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEv
   if (p.keys_per_split % 64) return hipErrorInvalidValue;
   const dim3 grid(p.nrb * p.KV, p.splits);
   if (dtype == 0) {
-    if (p.hd == 64) launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1, p);
-    else if (p.hd == 128) launch_k(attention_mfma_kernel<128, 8>, grid, dim3(64 * 8), 0, s, e0, e1, p);
-    else return hipErrorInvalidValue;
+    const bool split = p.splits > 1;
+    hipEvent_t e1a = split ? nullptr : e1;
+    if (p.hd == 64) {
+      launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
+      if (split) launch_k(attn_merge_kernel<bf16_t, 64>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
+    } else if (p.hd == 128) {
+      launch_k(attention_mfma_kernel<128, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
+      if (split) launch_k(attn_merge_kernel<bf16_t, 128>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
+    } else {
+      return hipErrorInvalidValue;
+    }
     return hipGetLastError();
   }
   if (p.hd == 64) return launch_attn_t<float, 64>(p, s, e0, e1);

@@ -204,7 +204,7 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
         const int hd = rp.hd, half = hd / 2, Nq = rp.H * hd, Nqk = Nq + rp.KV * hd;
         const int off = pos & 15;
         T* kv = (T*)rp.kv;
-        const size_t kblk = (size_t)max(blk, 0) * 2 * rp.KV * 16 * hd, vblk = kblk + (size_t)rp.KV * 16 * hd;
+        const int bk = max(blk, 0);
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
           const int c0 = n0 + 16 * j;           // first column of the tile
@@ -218,10 +218,10 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
             const float y = r16 < 8 ? a * cs.x - b * cs.y : a * cs.y + b * cs.x;
             if (h < rp.H) rp.q[(size_t)m * Nq + (size_t)h * hd + d] = y;
             else if (blk >= 0)
-              Store<T>::store(kv, kblk + (size_t)(h - rp.H) * 16 * hd + kv_key_off<T>(off, d, hd), y);
+              Store<T>::store(kv, kv_tile_off(h - rp.H, bk, 0, rp.nblk, hd) + kv_key_off<T>(off, d, hd), y);
           } else if (blk >= 0) {
             const int cv = c0 + r16 - Nqk;
-            Store<T>::store(kv, vblk + (size_t)(cv / hd) * 16 * hd + (size_t)(cv % hd) * 16 + off, o[j]);
+            Store<T>::store(kv, kv_tile_off(cv / hd, bk, 1, rp.nblk, hd) + kv_val_off<T>(off, cv % hd, hd), o[j]);
           }
         }
       } else if constexpr (EPI == EPI_SWIGLU) {

@@ -48,8 +48,7 @@ struct Lane {
   int part_rows = 0;
   float *attn_o = nullptr, *attn_ml = nullptr;
   size_t attn_o_cap = 0, attn_ml_cap = 0;
-  int* attn_cnt = nullptr;
-  int attn_cnt_n = 0;
+  int attn_items = 0;           // (row block, kv head) items the split partials hold
 };
 
 struct Slot {
@@ -194,12 +193,11 @@ void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int q
   ln.part_rows = std::min(rows, GEMM_MROWS);
   ln.part = al.take<float>(sizeof(float) * MAX_KSPLIT * ln.part_rows * D.d);
   ln.logits = logits_rows ? al.take<float>(sizeof(float) * logits_rows * D.V) : nullptr;
-  ln.attn_cnt_n = decode_rb * D.KV;
-  ln.attn_o_cap = (size_t)ln.attn_cnt_n * splits * qmax_dec * D.hd;
-  ln.attn_ml_cap = (size_t)ln.attn_cnt_n * splits * qmax_dec * 2;
+  ln.attn_items = decode_rb * D.KV;
+  ln.attn_o_cap = (size_t)ln.attn_items * splits * qmax_dec * D.hd;
+  ln.attn_ml_cap = (size_t)ln.attn_items * splits * qmax_dec * 2;
   ln.attn_o = al.take<float>(sizeof(float) * ln.attn_o_cap);
   ln.attn_ml = al.take<float>(sizeof(float) * ln.attn_ml_cap);
-  ln.attn_cnt = al.take<int>(sizeof(int) * std::max(1, ln.attn_cnt_n));
 }
 
 // prefill rows per attention row block: as many as fit the 64 query vectors
@@ -409,6 +407,7 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     rp.H = c.n_heads;
     rp.KV = c.n_kv_heads;
     rp.hd = c.head_dim;
+    rp.nblk = m.n_blocks;
     int rc = gemm(ctx, m, EPI_QKV, ln.xn, m.wqkv[l], M, m.nqkv(), d, nullptr, 0, nullptr, s, pk_all, -1, &rp);
     if (rc) return rc;
     AttnParams ap{};
@@ -416,6 +415,7 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.kv = rp.kv;
     ap.block_table = bt;
     ap.mbps = ctx->mbps;
+    ap.nblk = m.n_blocks;
     ap.row_pos = ln.row_pos;
     ap.row_slot = ln.row_slot;
     ap.rowblocks = rowblocks;
@@ -424,10 +424,8 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.H = c.n_heads;
     ap.KV = c.n_kv_heads;
     ap.hd = c.head_dim;
-    // split the keys only when the (row block, kv head) items leave more than
-    // half of the 256 compute units idle: a split costs a device-scope release
-    // per workgroup, which on MI355X (measured at 128 items, 8-wave
-    // workgroups) costs more than the idle units
+    // split the keys when the (row block, kv head) items leave more than half
+    // of the 256 compute units idle; the splits are merged by a second kernel
     int splits = attn_splits;
     const int items = nrb * c.n_kv_heads;
     if (items >= 128) splits = 1;
@@ -440,7 +438,6 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.out = ln.att;
     ap.part_o = ln.attn_o;
     ap.part_ml = ln.attn_ml;
-    ap.counters = ln.attn_cnt;
     ap.qmax = qmax;
     ProfRec ra;
     prof_begin(ctx, s, ra, verify ? SD_PROF_ATTN_VERIFY : -1, -1, 0, true);
@@ -542,7 +539,7 @@ int sd_init(const sd_config* cfg, const sd_weights* target, const sd_weights* dr
   ctx->slots.resize(cfg->max_slots);
   for (int b = cfg->kv_blocks_target - 1; b >= 0; --b) ctx->free_t.push_back(b);
   for (int b = cfg->kv_blocks_draft - 1; b >= 0; --b) ctx->free_d.push_back(b);
-  // device state: zero counters, invalid slots, no errors; rotary tables
+  // device state: invalid slots, no errors; rotary tables
   // (kernels, synchronous here)
   hipStream_t s = nullptr;
   bool ok = launch_fill_i32((int32_t*)cfg->workspace, 0, layout(cfg, nullptr) / 4, s) == hipSuccess &&

@@ -28,6 +28,13 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
 // l = 16 * (k-group) + r % 16, the 16 bytes of row r, k-group (k % step) /
 // (elements per 16 bytes).  Every 16-byte lane load of an operand fragment
 // is then part of one contiguous 1 KB block.
+// Element offset of the K (kv = 0) or V (kv = 1) tile of (kv head h, block b)
+// in one layer's pool.  The pool is head-major, [kv heads][blocks][K|V][16 x hd],
+// so the blocks of one task and head, allocated in order, form one run.
+__host__ __device__ __forceinline__ size_t kv_tile_off(int h, int b, int kv, int nblk, int hd) {
+  return (((size_t)h * nblk + b) * 2 + kv) * 16 * (size_t)hd;
+}
+
 // Element offset of key (token t, dim d) inside one 16-token block of one kv
 // head.  bf16 caches use the layout of the attention's matrix instruction:
 // for each of the hd/32 k-steps s, a 1 KB run of 64 16-byte units, unit
@@ -39,6 +46,19 @@ template <typename T> __host__ __device__ __forceinline__ int kv_key_off(int t, 
     return ((s * 4 + g) * 16 + t) * 8 + (d & 7);
   } else {
     return t * hd + d;
+  }
+}
+
+// Element offset of value (token t, dim d) inside one 16-token V tile.  bf16
+// caches: for each 32-dim group the 16 x 32 slice is ordered
+// [dim % 16][t / 4][(d / 16) % 2][t % 4], so that the 4 consecutive tokens of
+// two dims 16 apart are one 16-byte unit and a wave load of 64 such units is
+// one contiguous 1 KB.  fp32 caches: transposed, [hd][16].
+template <typename T> __host__ __device__ __forceinline__ int kv_val_off(int t, int d, int hd) {
+  if constexpr (sizeof(T) == 2) {
+    return ((((d >> 5) * 16 + (d & 15)) * 4 + (t >> 2)) * 2 + ((d >> 4) & 1)) * 4 + (t & 3);
+  } else {
+    return d * 16 + t;
   }
 }
 
@@ -111,11 +131,11 @@ struct NormParams {
 // halves of a pair meet in one lane.
 struct RopeParams {
   float* q;                    // [M, H hd] fp32, rotary applied
-  void* kv;                    // layer base of the pool: [blocks, 2, KV, 16, hd], V blocks as [hd][16]
+  void* kv;                    // layer base of the pool (kv_tile_off), V tiles as [hd][16]
   const float2* tab;           // [positions, hd/2] (cos, sin), fp64 angles rounded to fp32
   const int32_t* row_pos;      // [M]; -1 = inactive row
   const int32_t* row_blk;      // [M] KV block of the row's position; -1 = not written
-  int H, KV, hd;
+  int H, KV, hd, nblk;         // nblk: blocks in the pool
 };
 
 struct GemmParams {
@@ -130,9 +150,9 @@ struct GemmParams {
 
 struct AttnParams {
   const float* q;            // [M, H hd] (rotary applied)
-  const void* kv;            // layer base of the pool
+  const void* kv;            // layer base of the pool (kv_tile_off)
   const int32_t* block_table;
-  int mbps;
+  int mbps, nblk;            // block-table width, blocks in the pool
   const int32_t* row_pos;
   const int32_t* row_slot;
   const int32_t* rowblocks;  // [nrb, 2] = (row0, nrows), or null: rowblock i = rows [i*R, i*R+R)
@@ -142,7 +162,6 @@ struct AttnParams {
   void* out;                 // [M, H hd] model dtype, MFMA-tile layout
   float* part_o;             // [nrb*KV, splits, Qmax, hd]
   float* part_ml;            // [nrb*KV, splits, Qmax, 2]
-  int* counters;             // [nrb*KV]
   int qmax;                  // max query vectors per (rowblock, kv head)
 };
 
@@ -198,7 +217,7 @@ hipError_t launch_rmsnorm(int dtype, const NormParams& p, hipStream_t s);
 template <typename K, typename... A>
 inline void launch_k(K kern, dim3 grid, dim3 block, uint32_t shm, hipStream_t s, hipEvent_t e0, hipEvent_t e1,
                      A... args) {
-  if (e0) hipExtLaunchKernelGGL(kern, grid, block, shm, s, e0, e1, 0, args...);
+  if (e0 || e1) hipExtLaunchKernelGGL(kern, grid, block, shm, s, e0, e1, 0, args...);
   else hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
 }
 
