@@ -8,13 +8,15 @@
 //     sd_pack_linear, A written that way by the producing kernels), so every
 //     fragment load of a wave is one contiguous 1 KB block;
 //   * a workgroup owns one column tile (16*NT output columns = 16*NT rows
-//     of W; NT in {1, 2, 4}, wider tiles re-read the activations less
-//     often) and splits K over its KW waves (up to 16); each wave streams its
-//     K slice of the tile straight into registers, one step group ahead of
-//     the MFMAs;
+//     of W; NT in {1, 2, 3, 4}, wider tiles re-read the activations less
+//     often) and splits K over its KW waves (up to 16), interleaved in
+//     groups of U k-steps; each wave streams its share of the tile straight
+//     into registers, one step group ahead of the MFMAs;
 //   * the matching activation fragments are loaded the same way (they are
 //     small and stay in L2), so the main loop has no LDS traffic and no
-//     barriers, and vmcnt only ever waits for the older step group;
+//     barriers; it has no branches either (padding rows and groups past a
+//     wave's share are out-of-range buffer loads that return zero), so
+//     vmcnt only ever waits for the older step group;
 //   * bf16: one v_mfma_f32_16x16x32_bf16 per 16-byte unit; fp32: four
 //     v_mfma_f32_16x16x4_f32;
 //   * the KW partial tiles are added in wave order through LDS
@@ -66,16 +68,35 @@ template <int MT, int NT> struct GemmBounds {
 };
 int gemm_max_waves(int mt, int nt) { return (mt * nt <= 4 && mt < 4 && nt < 4) ? 16 : 8; }
 
+// Buffer resource over `bytes` bytes at p: raw (unswizzled) addressing with
+// range checking, so a load at an offset >= bytes returns zero and reads no
+// memory.  The main loop uses such offsets for padding rows and for step
+// groups past a wave's share instead of branches: a load under a branch makes
+// the compiler wait for every outstanding load before the next MFMA, which
+// serialises the stream.
+constexpr uint32_t OOB = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte buffer load; NT: non-temporal (streamed once, not kept in the caches)
+template <bool NT> __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, NT ? 2 : 0));
+}
+
 // Both operands are in the MFMA-tile layout (Tile<T>): fragment (tile t,
 // k-step s) of a lane is the 16-byte unit 64 (t * ksteps + s) + lane, so a
-// wave's load of one fragment is a contiguous 1 KB block.  A wave walks its
-// share of the k-steps in groups of U, starting at a workgroup-dependent
-// rotation that spreads concurrent activation reads over the L2 channels.
+// wave's load of one fragment is a contiguous 1 KB block.  The k-steps of a
+// workgroup's K range are taken in groups of U; wave w takes groups w, w + KW,
+// w + 2 KW, ..., so the waves of a workgroup read adjacent memory at any time.
+// Each wave keeps the next group's loads in flight while it multiplies the
+// current one (two register stages; scheduling barriers keep the compiler
+// from pulling the loads next to their uses).
 template <typename T, int MT, int NT, int U, int EPI>
 __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(GemmParams p) {
   __shared__ float red[4][MT * NT * 4][64];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int KW = blockDim.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int ksteps = (int)((size_t)p.K * sizeof(T) / 64);
@@ -83,14 +104,12 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
   // gridDim.y takes step groups [gb, gb + groups)
   const int gall = ksteps / U, gsp = (gall + gridDim.y - 1) / gridDim.y;
   const int gb = min((int)blockIdx.y * gsp, gall), groups = min(gsp, gall - gb);
-  const int per = (groups + KW - 1) / KW;
-  const int wc0 = min(wave * per, groups), wc1 = min(wc0 + per, groups);
-  const int nw = wc1 - wc0;
-  const int rot = nw > 0 ? (int)((blockIdx.x * 7u) % (unsigned)nw) : 0;
+  const int nw = max(0, (groups - wave + KW - 1) / KW);   // groups of this wave
   const int n0 = blockIdx.x * 16 * NT;
   const int m0 = blockIdx.z * MT * 16;
-  const u32x4* wp = (const u32x4*)p.W + (size_t)blockIdx.x * NT * ksteps * 64 + lane;
-  const u32x4* ap = (const u32x4*)p.A + (size_t)blockIdx.z * MT * ksteps * 64 + lane;
+  const uint32_t tile_bytes = (uint32_t)ksteps * 1024u;
+  const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)p.W + (size_t)blockIdx.x * NT * tile_bytes, NT * tile_bytes);
+  const __amdgpu_buffer_rsrc_t ar = buf_rsrc((const char*)p.A + (size_t)blockIdx.z * MT * tile_bytes, MT * tile_bytes);
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -98,26 +117,26 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  bool arow[MT];
+  // activation rows at or past M are padding: never read (their outputs are dropped)
+  uint32_t aoff[MT];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) arow[t] = m0 + 16 * t + r16 < p.M;
+  for (int t = 0; t < MT; ++t) aoff[t] = m0 + 16 * t + r16 < p.M ? (uint32_t)t * tile_bytes + lane * 16u : OOB;
   u32x4 ws[2][NT][U], as[2][MT][U];
   auto load = [&]<int S>(int i) {              // i-th step group of this wave's share
-    int c = wc0 + i + rot;
-    if (c >= wc1) c -= nw;
-    const int s0 = (gb + c) * U;
+    const bool ok = i < nw;
+    const uint32_t kb = (uint32_t)((gb + i * KW + wave) * U) * 1024u;
     // weights are read once: non-temporal loads keep them from evicting the
     // activations, which every workgroup re-reads from L2
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int u = 0; u < U; ++u) ws[S][j][u] = __builtin_nontemporal_load(&wp[((size_t)j * ksteps + s0 + u) * 64]);
-    // activation rows at or past M are padding: not loaded (their outputs are dropped)
+      for (int u = 0; u < U; ++u)
+        ws[S][j][u] = buf_load16<true>(wr, ok ? j * tile_bytes + kb + u * 1024u + lane * 16u : OOB);
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
-      for (int u = 0; u < U; ++u)
-        as[S][t][u] = arow[t] ? ap[((size_t)t * ksteps + s0 + u) * 64] : u32x4{0u, 0u, 0u, 0u};
+      for (int u = 0; u < U; ++u) as[S][t][u] = buf_load16<false>(ar, ok ? aoff[t] + kb + u * 1024u : OOB);
+    __builtin_amdgcn_sched_barrier(0);
   };
   auto compute = [&]<int S>() {
 #pragma unroll
@@ -126,17 +145,16 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
       for (int t = 0; t < MT; ++t)
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[t][j] = Mfma<T>::step(as[S][t][u], ws[S][j][u], acc[t][j]);
+    __builtin_amdgcn_sched_barrier(0);
   };
 
-  if (nw > 0) {
-    load.template operator()<0>(0);
-    for (int i = 0; i < nw; i += 2) {
-      if (i + 1 < nw) load.template operator()<1>(i + 1);
-      compute.template operator()<0>();
-      if (i + 1 >= nw) break;
-      if (i + 2 < nw) load.template operator()<0>(i + 2);
-      compute.template operator()<1>();
-    }
+  // groups past nw load zeros (no memory access) and add nothing
+  load.template operator()<0>(0);
+  for (int i = 0; i < nw; i += 2) {
+    load.template operator()<1>(i + 1);
+    compute.template operator()<0>();
+    load.template operator()<0>(i + 2);
+    compute.template operator()<1>();
   }
 
   // Reduction over the KW wave partials, in a fixed order: waves 4.. fold

@@ -283,19 +283,24 @@ struct GemmPlan {
 };
 
 // One column tile of 16*nt columns per workgroup, kw waves splitting K inside
-// it.  Chosen from sweeps on MI355X with packed operands at M = 40 and M = 8
-// (7B-shape verify and draft passes, weights streamed from HBM):
-//   * SwiGLU gate/up: 32-column tiles, 8 waves;
-//   * QKV: 16-column tiles at M <= 16; else 48-column tiles (at 7B, 256
-//     workgroups = one per CU: 23 us against 25 us for 64-column tiles on
-//     192 workgroups);
-//   * LM head (and QKV where 48 does not divide N): 64-column tiles with 6
-//     waves when that leaves ~170+ workgroups, else 32-column tiles;
-//   * residual projections (O, down), M <= 64 with an RMSNorm after them
-//     (split_ok): few column tiles, so K is split over workgroups until
-//     there are ~256 of them (32-column tiles at M > 16); the partial sums
-//     go through the workspace to the RMSNorm, which adds them to the
-//     residual stream.  Without split_ok the output is added in place.
+// it (interleaved step groups).  Chosen from sweeps on MI355X with packed
+// operands and weights streamed from HBM, at the verify and draft shapes of
+// the 7B-, 13B- and small configurations (M = 5 ... 320):
+//   * 4 waves per workgroup throughout (8 or 16 were never better by more
+//     than noise, often worse);
+//   * QKV: 48-column tiles when that gives 192 ... 320 workgroups (7B width:
+//     one per CU, 20 us against 25 us for 32-column tiles), else 16-column;
+//   * SwiGLU gate/up: 64-column tiles for 3-tile row blocks with < 512
+//     column pairs (fewer activation re-reads), else 32-column;
+//   * residual projections (O, down) with an RMSNorm after them (split_ok)
+//     and one row block: K split over workgroups until there are ~256 of
+//     them, 32-column tiles when every wave still gets >= 4 step groups,
+//     else 16-column; the partial sums go through the workspace to the
+//     RMSNorm, which adds them to the residual stream.  Without split_ok the
+//     output is added in place;
+//   * LM head and other stores: 64-column tiles for 3-tile row blocks, else
+//     32-column (4-tile row blocks take at most 32 columns);
+//   * several 64-row blocks (B >= 32 verify, prefill): 32-column tiles.
 // K is never split with a cross-workgroup reduction inside the GEMM: that
 // needs a device-scope release per workgroup, which costs more than it saves.
 GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = false) {
@@ -303,26 +308,27 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
   g.gz = (M + GEMM_MROWS - 1) / GEMM_MROWS;
   g.mt = g.gz > 1 ? 4 : (M + 15) / 16;
   g.ksplit = 1;
-  g.kw = 8;
+  g.kw = 4;
   const int groups = (int)(K * esz / 64) / GEMM_U;   // k-step groups of one wave step
-  if (epi == EPI_SWIGLU) {
-    g.nt = 2;
-  } else if (epi == EPI_QKV && g.mt == 1) {
-    g.nt = 1;                                         // draft-sized M: most workgroups
-  } else if (epi == EPI_QKV && g.mt <= 3 && N % 48 == 0 && N / 48 <= 320) {
-    g.nt = 3;                                         // up to ~one workgroup per CU
-  } else if (epi == EPI_RESID && split_ok && g.gz == 1) {
-    g.nt = (g.mt >= 2 && N % 32 == 0) ? 2 : 1;
-    const int gx = N / (16 * g.nt);
-    g.ksplit = std::min(std::min(MAX_KSPLIT, std::max(1, (256 + gx - 1) / gx)), std::max(1, groups / 4));
-    if (g.ksplit == 1 && g.nt == 2) g.nt = 1;
-  } else if (g.mt <= 3 && N % 64 == 0 && N / 64 >= 170) {
-    g.nt = 4;                                         // 64-row blocks take at most 32 columns
-    g.kw = 6;
-  } else if (N % 32 == 0 && N / 32 >= 170) {
-    g.nt = 2;
-  } else {
+  auto pick = [&](int nt) { return N % (16 * nt) == 0; };
+  if (g.gz > 1) {
+    g.nt = pick(2) ? 2 : 1;
+  } else if (epi == EPI_SWIGLU) {
+    g.nt = (g.mt == 3 && pick(4) && N / 32 < 512) ? 4 : 2;
+  } else if (epi == EPI_QKV) {
+    g.nt = (g.mt <= 3 && pick(3) && N / 48 >= 192 && N / 48 <= 320) ? 3 : 1;
+  } else if (epi == EPI_RESID && split_ok) {
+    auto splits = [&](int nt) {
+      const int gx = N / (16 * nt);
+      return std::min(std::min(MAX_KSPLIT, std::max(1, (256 + gx - 1) / gx)), std::max(1, groups / 4));
+    };
     g.nt = 1;
+    if (g.mt >= 2 && pick(2) && groups / splits(2) >= 4 * g.kw) g.nt = 2;
+    g.ksplit = splits(g.nt);
+  } else if (g.mt == 3 && pick(4)) {
+    g.nt = 4;
+  } else {
+    g.nt = pick(2) ? 2 : 1;
   }
   g.gx = N / (16 * g.nt);
   const int gps = (groups + g.ksplit - 1) / g.ksplit;
