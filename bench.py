@@ -35,8 +35,8 @@ METRIC = "verified tokens/sec + verify-step latency, 7B-shape bf16 B=8 gamma=4; 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="7b_b8", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch size")
     ap.add_argument("--gamma", type=int, default=0, help="override the workload's gamma")
@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--pmc-pass", action="store_true",
                     help="short eager run for rocprofv3 --pmc: a 1 GiB copy kernel (counter calibration) "
                          "and two eager steps, no JSON line")
+    ap.add_argument("--trace-summary", metavar="KERNEL_TRACE_CSV",
+                    help="summarise a rocprofv3 --kernel-trace csv of a default bench run (whole run by kernel, "
+                         "and the median timed step by kernel and launch shape) as markdown and exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc counter_collection.csv files of --pmc-pass runs "
                          "(FETCH_SIZE, then WRITE_SIZE) into profiles/pmc_traffic.json and exit")
@@ -176,10 +179,102 @@ def cpu_baseline(wl, B, gamma, emitted_per_step):
             "step_seconds": round(t_step, 4)}
 
 
+def trace_summary(path: str, warmup: int, steps: int) -> None:
+    """Markdown summary of a rocprofv3 kernel trace of a default bench run.
+    The timed steps are graph replays W .. W+K-1; a step runs from the first
+    dispatch after the previous step's commit_kernel to its own
+    commit_kernel (the prefill issues none)."""
+    import csv
+    from collections import defaultdict
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"],
+                         int(r.get("Grid_Size_X", r.get("Grid_Size", 0)) or 0),
+                         int(r.get("Workgroup_Size_X", r.get("Workgroup_Size", 0)) or 0),
+                         int(r.get("Grid_Size_Y", 1) or 1)))
+    rows.sort()
+
+    def short(n):
+        # "void sd::gemm_kernel<...>(sd::GemmParams) [clone .kd]" -> "sd::gemm_kernel<...>"
+        n = n.split(" [clone")[0].strip()
+        if n.startswith("void "):
+            n = n[5:]
+        if n.endswith(")"):
+            depth = 0
+            for i in range(len(n) - 1, -1, -1):
+                depth += n[i] == ")"
+                depth -= n[i] == "("
+                if depth == 0:
+                    n = n[:i]
+                    break
+        return n
+
+    tot = defaultdict(list)
+    for s, e, n, *_ in rows:
+        tot[short(n)].append((e - s) / 1e3)
+    all_us = sum(sum(v) for v in tot.values())
+    print("## Whole run: every dispatch of the command\n")
+    print("| kernel | calls | total ms | avg us | min us | max us | % |\n|---|---:|---:|---:|---:|---:|---:|")
+    for n, v in sorted(tot.items(), key=lambda kv: -sum(kv[1])):
+        print(f"| `{n[:90]}` | {len(v)} | {sum(v) / 1e3:.2f} | {np.mean(v):.2f} | {min(v):.2f} | {max(v):.2f} "
+              f"| {100 * sum(v) / all_us:.1f} |")
+    ends = [i for i, r in enumerate(rows) if "commit_kernel" in r[2]]
+    spans = []
+    for k in range(warmup, warmup + steps):
+        if k < 1 or k >= len(ends):
+            continue
+        spans.append((ends[k - 1] + 1, ends[k]))
+    if not spans:
+        return
+    dur = [rows[b][1] - rows[a][0] for a, b in spans]
+    med = spans[int(np.argsort(dur)[len(dur) // 2])]
+    a, b = med
+    step = defaultdict(list)
+    for s, e, n, gx, wg, gy in rows[a:b + 1]:
+        step[f"{short(n)[:80]}  grid {gx}x{gy}, wg {wg}"].append((e - s) / 1e3)
+    print(f"\n## One timed step (graph replay; median span of {len(spans)} timed steps): "
+          f"{(rows[b][1] - rows[a][0]) / 1e3:.1f} us, {b - a + 1} dispatches, "
+          f"kernel busy {sum(sum(v) for v in step.values()):.1f} us\n")
+    print("| kernel (launch shape) | calls/step | total us | avg us | median us |\n|---|---:|---:|---:|---:|")
+    for n, v in sorted(step.items(), key=lambda kv: -sum(kv[1])):
+        print(f"| `{n}` | {len(v)} | {sum(v):.1f} | {np.mean(v):.2f} | {np.median(v):.2f} |")
+
+
+def graph_latencies(eng, batch, u_step, n):
+    """Median-ready lists of n replay times (ms) of the verify pass and of the
+    gamma draft calls of one batch, each captured as a HIP graph."""
+    import torch
+    from paper_2510_11331_amd.engine import uniforms_device
+    u = uniforms_device(u_step)
+    gv, gd = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gv):
+        eng.verify(batch)
+    with torch.cuda.graph(gd):
+        for i in range(batch.gamma):
+            eng.draft_step(batch, i, u)
+    out = []
+    for g in (gv, gd):
+        g.replay()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        ev[0].record()
+        for k in range(n):
+            g.replay()
+            ev[k + 1].record()
+        torch.cuda.synchronize()
+        out.append(np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(n)]))
+    del gv, gd
+    return out
+
+
 def main():
     args = parse()
     if args.traffic_from:
         summarise_counters(*args.traffic_from)
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary, args.warmup, args.steps)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
@@ -259,26 +354,28 @@ def main():
     value = emitted / elapsed
     print(f"[bench] timed {K} steps in {elapsed:.3f}s, {emitted} tokens", file=sys.stderr, flush=True)
 
-    # instrumented pass: HIP events on the launch stream around each kernel
-    # class.  Each step is queued behind a GPU sleep longer than its host
-    # enqueue time, so the events time kernels, not host launch latency.
+    # verify-step and draft-call latency: the verify pass alone (and the gamma
+    # draft calls alone) captured as HIP graphs and replayed back to back,
+    # HIP events on the replay stream around every replay.  A replay repeats
+    # the same work (same rows, same K/V written at the same uncommitted
+    # positions), so every replay is one verify step of this batch.
+    verify_ms, draft_ms = graph_latencies(eng, batch, ut[W + K - 1], K)
+
+    # instrumented pass: dispatch-stamped HIP events around the GEMM and
+    # attention kernels.  Each step is queued behind a GPU sleep longer than
+    # its host enqueue time, so the events time kernels, not launch latency.
     s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s0.record(); torch.cuda._sleep(1_000_000); s1.record(); torch.cuda.synchronize()
     cycles_per_ms = 1_000_000 / max(s0.elapsed_time(s1), 1e-3)
     eng.profile(True)
-    verify_ms = []
     for n in range(K):
         torch.cuda._sleep(int(cycles_per_ms * 40))
         generate(eng, [batch], [ut[W + K + n:W + K + n + 1]], 1, two_streams=False)
-        c, ms, _ = eng.profile_read(_lib.SD_PROF_VERIFY)
-        verify_ms.append(ms / max(c, 1))
     n_gu, ms_gu, bytes_gu = eng.profile_read(_lib.SD_PROF_GEMM_VERIFY_GATEUP)
     n_all, ms_all, bytes_all = eng.profile_read(_lib.SD_PROF_GEMM_VERIFY_ALL)
     n_at, ms_at, _ = eng.profile_read(_lib.SD_PROF_ATTN_VERIFY)
-    n_dr, ms_dr, _ = eng.profile_read(_lib.SD_PROF_DRAFT)
     eng.profile(False)
     flags = eng.check_flags()
-    verify_ms = np.array(verify_ms)
     gu_ms = ms_gu / max(n_gu, 1)
     gu_bytes = bytes_gu / max(n_gu, 1)
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
@@ -319,7 +416,7 @@ def main():
         "verify_hbm_frac": round(step_bytes / (verify_p50 * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "verify_gemm_gbs": round(bytes_all / max(ms_all, 1e-9) * 1e-6, 1),
         "verify_attn_ms_per_layer": round(ms_at / max(n_at, 1), 4),
-        "draft_ms_per_call": round(ms_dr / max(n_dr, 1), 4),
+        "draft_ms_per_call": round(float(np.median(draft_ms)) / gamma, 4),
         "mean_accepted": round(float(acc.mean()), 4),
         "mean_emitted_per_step": round(float((acc + 1).mean()), 4),
         "device_flags": flags,

@@ -105,7 +105,7 @@ typedef struct {
     int max_slots;          /* task slots                                   */
     int max_batch;          /* max tasks per draft/verify call              */
     int gamma_max;          /* max speculation length (1..16)               */
-    int max_ctx;            /* max positions a slot may reach               */
+    int max_ctx;            /* max positions a slot may reach (<= 32768)    */
     int kv_block;           /* tokens per KV block; must be 16              */
     int kv_blocks_target;   /* blocks in the target pool                    */
     int kv_blocks_draft;    /* blocks in the draft pool                     */

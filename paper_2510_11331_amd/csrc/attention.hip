@@ -265,7 +265,10 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
   __shared__ float s_o[NSLOT][16][HD + 4];
   __shared__ float s_m[NSLOT][16], s_l[NSLOT][16];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ int s_bt[ATTN_BT_CAP];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const int rbk = blockIdx.x;
   const int rb = rbk / p.KV, kvh = rbk % p.KV;
@@ -286,11 +289,22 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
   const int qt = wave % QTe, kg = wave / QTe;
   const bool wave_on = qt < QT;
 
-  int maxpos = -1;
-  for (int r = 0; r < nr; ++r) maxpos = max(maxpos, p.row_pos[row0 + r]);
+  // the block's rows (nr <= 64: Qn is at most 64 query vectors) in parallel
+  int maxpos = lane < nr ? p.row_pos[row0 + lane] : -1;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) maxpos = max(maxpos, __shfl_xor(maxpos, o));
+  maxpos = __builtin_amdgcn_readfirstlane(maxpos);
   const int slot = p.row_slot[row0];
   const int k_begin = split * p.keys_per_split;
   const int k_end = min(min(k_begin + p.keys_per_split, maxpos + 1), p.mbps * 16);
+
+  // block ids of the split's key range, staged in LDS (the host keeps a
+  // split within ATTN_BT_CAP blocks): a key load then never waits on the
+  // memory counter behind the keys still in flight
+  const int32_t* bt = p.block_table + (size_t)slot * p.mbps;
+  const int bfirst = k_begin / 16, nbr = max(0, (k_end + 15) / 16 - bfirst);
+  for (int i = tid; i < min(nbr, ATTN_BT_CAP); i += blockDim.x) s_bt[i] = bt[bfirst + i];
+  __syncthreads();
 
   const int qi = qt * 16 + r16;
   const bool qvalid = wave_on && qi < Qn;
@@ -300,12 +314,16 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
 
   u32x4 qhi[UPG], qlo[UPG];
   {
-    const float* qs = p.q + (size_t)qrow * p.H * HD + (size_t)qh * HD + g * (HD / 4);
+    // always-valid address (row0, head kvh G for idle lanes), zeroed after the load
+    const float4* qs = (const float4*)(p.q + (size_t)qrow * p.H * HD + (size_t)qh * HD + g * (HD / 4));
+    float4 xv[2 * UPG];
+#pragma unroll
+    for (int s = 0; s < 2 * UPG; ++s) xv[s] = qs[s];
 #pragma unroll
     for (int s = 0; s < UPG; ++s) {
-      float x[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = qvalid ? qs[8 * s + e] * p.scale : 0.f;
+      const float sc = qvalid ? p.scale : 0.f;
+      float x[8] = {xv[2 * s].x * sc, xv[2 * s].y * sc, xv[2 * s].z * sc, xv[2 * s].w * sc,
+                    xv[2 * s + 1].x * sc, xv[2 * s + 1].y * sc, xv[2 * s + 1].z * sc, xv[2 * s + 1].w * sc};
       split8(x, qhi[s], qlo[s]);
     }
   }
@@ -315,43 +333,48 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
 #pragma unroll
   for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const bf16_t* kv = (const bf16_t*)p.kv;
-  const int32_t* bt = p.block_table + (size_t)slot * p.mbps;
+  // this kv head's region of the pool ([blocks][K|V][16 x HD], 2 x 16 HD
+  // bf16 per block) as a range-checked buffer: steps past the key range
+  // load at an out-of-range offset, which returns zero and reads nothing
+  constexpr uint32_t BLK_BYTES = 2u * 16u * HD * 2u;
+  const __amdgpu_buffer_rsrc_t kvr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>((const bf16_t*)p.kv + kv_tile_off(kvh, 0, 0, p.nblk, HD)), (short)0,
+      (int)((uint32_t)p.nblk * BLK_BYTES), 0x00020000);
   // key tile in the matrix-instruction layout: k-step s is the 1 KB run at
   // unit 64 s, this lane's 16 bytes at unit 64 s + lane (token r16, dims
   // g HD/4 + 8 s .. + 8); the V tile follows the K tile of the same block
-  const size_t koff = (size_t)lane * 8;
+  const uint32_t koff = (uint32_t)lane * 16u;
   // V tile (kv_val_off): unit 4 r16 + g of 32-dim group dp holds tokens
   // 4g..4g+3 of dims 32 dp + r16 and 32 dp + 16 + r16 (the 64 lanes read the
   // group's 1 KB)
-  const size_t voff = (size_t)16 * HD + (size_t)(4 * r16 + g) * 8;
+  const uint32_t voff = 16u * HD * 2u + (uint32_t)(4 * r16 + g) * 16u;
 
-  // two register stages of one 32-key step: K rows (two blocks) and V^T quads
-  u32x4 Kf[2][2][UPG];
-  uint32_t Vf[2][2][DT][2];
+  // two register stages of one 32-key step: K rows (two blocks), V^T quads
+  // as loaded, and the masks of the V entries past the key range (applied
+  // by the step, so a load is not consumed the moment it is issued)
+  u32x4 Kf[2][2][UPG], Vr[2][2][DT / 2];
+  uint32_t Vm[2][2][2];
 
   auto load = [&]<int S>(int kb) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const int bi = kb / 16 + t;
-      const bool ok = bi < p.mbps && kb + 16 * t < k_end;
-      const bf16_t* base = kv + kv_tile_off(kvh, ok ? bt[bi] : 0, 0, p.nblk, HD);
+      const int kt = kb + 16 * t;
+      const bool ok = kt < k_end;
+      const uint32_t base = ok ? (uint32_t)s_bt[kt / 16 - bfirst] * BLK_BYTES : 0x80000000u;
 #pragma unroll
-      for (int s = 0; s < UPG; ++s) Kf[S][t][s] = __builtin_nontemporal_load((const u32x4*)(base + koff + 512 * s));
+      for (int s = 0; s < UPG; ++s)
+        Kf[S][t][s] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kvr, base + koff + 1024u * s, 0, 2));
       // keys at or past k_end were never written: their scores are masked, and
       // their V entries are zeroed so that p = 0 never meets a NaN/Inf pattern
-      const int nq = min(max(k_end - (kb + 16 * t + 4 * g), 0), 4);
-      const uint32_t mx = nq >= 2 ? 0xffffffffu : (nq == 1 ? 0xffffu : 0u);
-      const uint32_t my = nq >= 4 ? 0xffffffffu : (nq == 3 ? 0xffffu : 0u);
+      const int nq = min(max(k_end - (kt + 4 * g), 0), 4);
+      Vm[S][t][0] = nq >= 2 ? 0xffffffffu : (nq == 1 ? 0xffffu : 0u);
+      Vm[S][t][1] = nq >= 4 ? 0xffffffffu : (nq == 3 ? 0xffffu : 0u);
 #pragma unroll
-      for (int dp = 0; dp < DT / 2; ++dp) {
-        const u32x4 v = __builtin_nontemporal_load((const u32x4*)(base + voff + (size_t)dp * 512));
-        Vf[S][t][2 * dp][0] = v.x & mx;
-        Vf[S][t][2 * dp][1] = v.y & my;
-        Vf[S][t][2 * dp + 1][0] = v.z & mx;
-        Vf[S][t][2 * dp + 1][1] = v.w & my;
-      }
+      for (int dp = 0; dp < DT / 2; ++dp)
+        Vr[S][t][dp] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(kvr, base + voff + 1024u * dp, 0, 2));
     }
+    __builtin_amdgcn_sched_barrier(0);
   };
   auto step = [&]<int S>(int kb) {
     f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
@@ -394,23 +417,28 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
 #pragma unroll
     for (int d = 0; d < DT; ++d) {
       o[d] *= alpha;
-      const u32x4 va = u32x4{Vf[S][0][d][0], Vf[S][0][d][1], Vf[S][1][d][0], Vf[S][1][d][1]};
+      // dims d (even d: x, y of the unit) of tokens 4g..4g+3 of both blocks
+      const u32x4 v0 = Vr[S][0][d / 2], v1 = Vr[S][1][d / 2];
+      const u32x4 va = (d & 1) ? u32x4{v0.z & Vm[S][0][0], v0.w & Vm[S][0][1], v1.z & Vm[S][1][0], v1.w & Vm[S][1][1]}
+                               : u32x4{v0.x & Vm[S][0][0], v0.y & Vm[S][0][1], v1.x & Vm[S][1][0], v1.y & Vm[S][1][1]};
       o[d] = mfma_bf16(va, phi, o[d]);
       o[d] = mfma_bf16(va, plo, o[d]);
     }
+    __builtin_amdgcn_sched_barrier(0);
   };
 
+  // loads are issued unconditionally (past the key range they read
+  // nothing), so the compiler keeps the next step in flight during a step
   const int kstep = 32 * KG;
   int kb = k_begin + 32 * kg;
   if (wave_on && kb < k_end) {
     load.template operator()<0>(kb);
     for (; kb < k_end; kb += 2 * kstep) {
       const int kb1 = kb + kstep;
-      if (kb1 < k_end) load.template operator()<1>(kb1);
+      load.template operator()<1>(kb1);
       step.template operator()<0>(kb);
       if (kb1 >= k_end) break;
-      const int kb2 = kb1 + kstep;
-      if (kb2 < k_end) load.template operator()<0>(kb2);
+      load.template operator()<0>(kb1 + kstep);
       step.template operator()<1>(kb1);
     }
   }
@@ -541,7 +569,7 @@ static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s, hipEvent_t e
 hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (p.nrb <= 0) return hipSuccess;
   if (p.qmax > ATTN_QMAX) return hipErrorInvalidValue;
-  if (p.keys_per_split % 64) return hipErrorInvalidValue;
+  if (p.keys_per_split % 64 || p.keys_per_split > ATTN_BT_CAP * 16) return hipErrorInvalidValue;
   const dim3 grid(p.nrb * p.KV, p.splits);
   if (dtype == 0) {
     const bool split = p.splits > 1;

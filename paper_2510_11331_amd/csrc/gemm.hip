@@ -148,6 +148,19 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     __builtin_amdgcn_sched_barrier(0);
   };
 
+  // QKV runs exactly 4 waves, so wave w finishes the rows 16 i + 4 g + w of
+  // the block; their positions and KV blocks are loaded before the stream
+  // and their rotary (cos, sin) after it, so the epilogue waits on nothing
+  int qpos[EPI == EPI_QKV ? MT : 1], qblk[EPI == EPI_QKV ? MT : 1];
+  if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int m = m0 + 16 * i + 4 * g + wave;
+      qpos[i] = m < p.M ? p.rope.row_pos[m] : -1;
+      qblk[i] = m < p.M ? p.rope.row_blk[m] : -1;
+    }
+  }
+
   // groups past nw load zeros (no memory access) and add nothing
   load.template operator()<0>(0);
   for (int i = 0; i < nw; i += 2) {
@@ -155,6 +168,18 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     compute.template operator()<0>();
     load.template operator()<0>(i + 2);
     compute.template operator()<1>();
+  }
+
+  float2 qcs[EPI == EPI_QKV ? MT : 1][NT];
+  if constexpr (EPI == EPI_QKV) {
+    const int half = p.rope.hd / 2;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int c0 = n0 + 16 * j, f = 8 * ((c0 % p.rope.hd) / 16) + (r16 & 7);
+        qcs[i][j] = qpos[i] >= 0 ? p.rope.tab[(size_t)qpos[i] * half + f] : float2{1.f, 0.f};
+      }
   }
 
   // Reduction over the KW wave partials, in a fixed order: waves 4.. fold
@@ -191,6 +216,46 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
         for (int v = 0; v < 4; ++v) red[wave][(i * NT + j) * 4 + v][lane] = acc[i][j][v];
   }
   __syncthreads();
+  if constexpr (EPI == EPI_QKV) {
+    // first use of the prefetched rotary inputs before any store: the wait
+    // for them is taken here, not behind the epilogue's stores (the memory
+    // counter also counts stores)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      asm volatile("" : "+v"(qpos[i]), "+v"(qblk[i]));
+#pragma unroll
+      for (int j = 0; j < NT; ++j) asm volatile("" : "+v"(qcs[i][j].x), "+v"(qcs[i][j].y));
+    }
+  }
+
+  // QKV: what column n0 + 16 j + r16 of this lane is, independent of the
+  // row: kind (0 q, 1 k, 2 v), q column, and the K/V element offset of
+  // (token 0, block 0) in the cache; a row adds its block and token offsets
+  int qkind[EPI == EPI_QKV ? NT : 1], qcol[EPI == EPI_QKV ? NT : 1];
+  size_t qkvb[EPI == EPI_QKV ? NT : 1];
+  const int Nq = p.rope.H * p.rope.hd;
+  if constexpr (EPI == EPI_QKV) {
+    const RopeParams& rp = p.rope;
+    const int hd = rp.hd, half = hd / 2, Nqk = Nq + rp.KV * hd;
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const int c0 = n0 + 16 * j;             // first column of the tile
+      qkind[j] = c0 < Nq ? 0 : c0 < Nqk ? 1 : 2;
+      qcol[j] = 0;
+      qkvb[j] = 0;
+      if (c0 < Nqk) {
+        // rotary pair order: column r16 < 8 of the tile is dim 8b + r16 of
+        // head h, column r16 + 8 its partner dim hd/2 + 8b + r16
+        const int h = c0 / hd, f = 8 * ((c0 % hd) / 16) + (r16 & 7);
+        const int d = r16 < 8 ? f : f + half;
+        if (h < rp.H) qcol[j] = h * hd + d;
+        else qkvb[j] = kv_tile_off(h - rp.H, 0, 0, rp.nblk, hd) + kv_key_off<T>(0, d, hd);
+      } else {
+        const int cv = c0 + r16 - Nqk;
+        qkvb[j] = kv_tile_off(cv / hd, 0, 1, rp.nblk, hd) + kv_val_off<T>(0, cv % hd, hd);
+      }
+    }
+  }
 
   // output element (i, j, v) is row m0 + 16 i + 4 g + v, column n0 + 16 j + r16
 #pragma unroll
@@ -215,31 +280,27 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
       }
       if (m >= p.M) continue;
       if constexpr (EPI == EPI_QKV) {
-        const RopeParams& rp = p.rope;
-        const int pos = rp.row_pos[m];
+        const int pos = qpos[i];                // this lane's row m (v == wave)
         if (pos < 0) continue;                  // row without an input (no pending draft token)
-        const int blk = rp.row_blk[m];          // -1: K/V not written (over capacity, flagged)
-        const int hd = rp.hd, half = hd / 2, Nq = rp.H * hd, Nqk = Nq + rp.KV * hd;
+        const int blk = qblk[i];                // -1: K/V not written (over capacity, flagged)
         const int off = pos & 15;
-        T* kv = (T*)rp.kv;
-        const int bk = max(blk, 0);
+        T* kv = (T*)p.rope.kv;
+        const size_t brow = (size_t)max(blk, 0) * 32 * p.rope.hd;   // block offset inside a head's run
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
-          const int c0 = n0 + 16 * j;           // first column of the tile
-          if (c0 < Nqk) {
-            // rotary pair order: column r16 < 8 of the tile is dim 8b + r16 of
-            // head h, column r16 + 8 its partner dim hd/2 + 8b + r16
-            const int h = c0 / hd, f = 8 * ((c0 % hd) / 16) + (r16 & 7);
-            const int d = r16 < 8 ? f : f + half;
-            const float2 cs = rp.tab[(size_t)pos * half + f];
+          if (qkind[j] == 0) {
+            const float2 cs = qcs[i][j];
             const float a = r16 < 8 ? o[j] : pr[j], b = r16 < 8 ? pr[j] : o[j];
-            const float y = r16 < 8 ? a * cs.x - b * cs.y : a * cs.y + b * cs.x;
-            if (h < rp.H) rp.q[(size_t)m * Nq + (size_t)h * hd + d] = y;
-            else if (blk >= 0)
-              Store<T>::store(kv, kv_tile_off(h - rp.H, bk, 0, rp.nblk, hd) + kv_key_off<T>(off, d, hd), y);
-          } else if (blk >= 0) {
-            const int cv = c0 + r16 - Nqk;
-            Store<T>::store(kv, kv_tile_off(cv / hd, bk, 1, rp.nblk, hd) + kv_val_off<T>(off, cv % hd, hd), o[j]);
+            p.rope.q[(size_t)m * Nq + qcol[j]] = r16 < 8 ? a * cs.x - b * cs.y : a * cs.y + b * cs.x;
+          } else if (qkind[j] == 1) {
+            if (blk < 0) continue;
+            const float2 cs = qcs[i][j];
+            const float a = r16 < 8 ? o[j] : pr[j], b = r16 < 8 ? pr[j] : o[j];
+            Store<T>::store(kv, qkvb[j] + brow + kv_key_off<T>(off, 0, p.rope.hd),
+                            r16 < 8 ? a * cs.x - b * cs.y : a * cs.y + b * cs.x);
+          } else {
+            if (blk < 0) continue;
+            Store<T>::store(kv, qkvb[j] + brow + kv_val_off<T>(off, 0, p.rope.hd), o[j]);
           }
         }
       } else if constexpr (EPI == EPI_SWIGLU) {
@@ -339,7 +400,8 @@ hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, i
     return hipErrorInvalidValue;
   dim3 grid(grid_x, ksplit, grid_z);
   const int threads = 64 * kw;
-  if (epi == EPI_QKV && (p.rope.hd % 16 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd)) return hipErrorInvalidValue;
+  if (epi == EPI_QKV && (kw != 4 || p.rope.hd % 16 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd))
+    return hipErrorInvalidValue;
   if (dtype == 0) {
     if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, p, s, e0, e1);
     if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, p, s, e0, e1);

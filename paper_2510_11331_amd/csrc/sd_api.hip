@@ -121,7 +121,7 @@ bool cfg_ok(const sd_config* c) {
   if (c->max_slots < 1 || c->max_batch < 1 || c->max_batch > c->max_slots) return false;
   if (c->gamma_max < 1 || c->gamma_max > 16) return false;
   if (c->kv_block != KV_BLOCK) return false;
-  if (c->max_ctx < 2 || c->kv_blocks_target < 1 || c->kv_blocks_draft < 1) return false;
+  if (c->max_ctx < 2 || c->max_ctx > MAX_CTX || c->kv_blocks_target < 1 || c->kv_blocks_draft < 1) return false;
   if (c->prefill_rows < 1) return false;
   if (!(c->temperature > 0.f)) return false;
   if ((c->target.n_heads / c->target.n_kv_heads) * (c->gamma_max + 1) > ATTN_QMAX) return false;
@@ -332,7 +332,8 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
   }
   g.gx = N / (16 * g.nt);
   const int gps = (groups + g.ksplit - 1) / g.ksplit;
-  g.kw = std::max(1, std::min(g.kw, gps / 2));
+  // the QKV epilogue assigns output rows by wave and needs exactly 4 waves
+  if (epi != EPI_QKV) g.kw = std::max(1, std::min(g.kw, gps / 2));
   return g;
 }
 

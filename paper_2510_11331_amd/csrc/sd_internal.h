@@ -243,5 +243,7 @@ constexpr int GEMM_MROWS = 64;         // rows per M block (4 MFMA row tiles)
 // attention geometry
 constexpr int ATTN_KEYS = 64;          // keys per LDS chunk
 constexpr int ATTN_QMAX = 64;          // max query vectors per workgroup
+constexpr int ATTN_BT_CAP = 2048;      // KV blocks of one key range staged in LDS (32768 positions)
+constexpr int MAX_CTX = ATTN_BT_CAP * 16;   // positions a slot may reach
 
 }  // namespace sd
