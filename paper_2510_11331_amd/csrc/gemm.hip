@@ -105,11 +105,23 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
   const int gall = ksteps / U, gsp = (gall + gridDim.y - 1) / gridDim.y;
   const int gb = min((int)blockIdx.y * gsp, gall), groups = min(gsp, gall - gb);
   const int nw = max(0, (groups - wave + KW - 1) / KW);   // groups of this wave
-  const int n0 = blockIdx.x * 16 * NT;
-  const int m0 = blockIdx.z * MT * 16;
+  // Several M blocks (p.mblocks > 1, 1-D grid): workgroup w runs on XCD w % 8
+  // (round-robin dispatch), so the M blocks of one column tile are given
+  // consecutive slots of one XCD; they run together and all but the first
+  // find the tile's weights in that XCD's L2 (plain loads, not streamed).
+  // Otherwise blockIdx.x is the column tile and blockIdx.z the M block.
+  int bx = blockIdx.x, bz = blockIdx.z;
+  if (p.mblocks > 1) {
+    const int w = blockIdx.x, j = w >> 3;
+    bz = j % p.mblocks;
+    bx = (j / p.mblocks) * 8 + (w & 7);
+  }
+  const bool stream_w = p.mblocks <= 1;
+  const int n0 = bx * 16 * NT;
+  const int m0 = bz * MT * 16;
   const uint32_t tile_bytes = (uint32_t)ksteps * 1024u;
-  const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)p.W + (size_t)blockIdx.x * NT * tile_bytes, NT * tile_bytes);
-  const __amdgpu_buffer_rsrc_t ar = buf_rsrc((const char*)p.A + (size_t)blockIdx.z * MT * tile_bytes, MT * tile_bytes);
+  const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)p.W + (size_t)bx * NT * tile_bytes, NT * tile_bytes);
+  const __amdgpu_buffer_rsrc_t ar = buf_rsrc((const char*)p.A + (size_t)bz * MT * tile_bytes, MT * tile_bytes);
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -130,8 +142,10 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int u = 0; u < U; ++u)
-        ws[S][j][u] = buf_load16<true>(wr, ok ? j * tile_bytes + kb + u * 1024u + lane * 16u : OOB);
+      for (int u = 0; u < U; ++u) {
+        const uint32_t o = ok ? j * tile_bytes + kb + u * 1024u + lane * 16u : OOB;
+        ws[S][j][u] = stream_w ? buf_load16<true>(wr, o) : buf_load16<false>(wr, o);
+      }
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
@@ -398,22 +412,29 @@ hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, i
     return hipErrorInvalidValue;
   if (ksplit < 1 || (ksplit > 1 && epi != EPI_PART) || ksplit > (int)((size_t)p.K * (dtype == 0 ? 2 : 4) / GEMM_CHUNK))
     return hipErrorInvalidValue;
+  // several M blocks over column tiles in groups of 8: the XCD-aware 1-D grid
+  GemmParams q = p;
+  q.mblocks = 1;
   dim3 grid(grid_x, ksplit, grid_z);
+  if (grid_z > 1 && ksplit == 1 && grid_x % 8 == 0) {
+    q.mblocks = grid_z;
+    grid = dim3(grid_x * grid_z, 1, 1);
+  }
   const int threads = 64 * kw;
   if (epi == EPI_QKV && (kw != 4 || p.rope.hd % 16 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd))
     return hipErrorInvalidValue;
   if (dtype == 0) {
-    if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, p, s, e0, e1);
-    if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, p, s, e0, e1);
-    if (epi == EPI_QKV) return launch_nt<bf16_t, EPI_QKV>(nt, mt, grid, threads, p, s, e0, e1);
-    if (epi == EPI_PART) return launch_nt<bf16_t, EPI_PART>(nt, mt, grid, threads, p, s, e0, e1);
-    return launch_nt<bf16_t, EPI_SWIGLU>(nt, mt, grid, threads, p, s, e0, e1);
+    if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, q, s, e0, e1);
+    if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, q, s, e0, e1);
+    if (epi == EPI_QKV) return launch_nt<bf16_t, EPI_QKV>(nt, mt, grid, threads, q, s, e0, e1);
+    if (epi == EPI_PART) return launch_nt<bf16_t, EPI_PART>(nt, mt, grid, threads, q, s, e0, e1);
+    return launch_nt<bf16_t, EPI_SWIGLU>(nt, mt, grid, threads, q, s, e0, e1);
   }
-  if (epi == EPI_STORE) return launch_nt<float, EPI_STORE>(nt, mt, grid, threads, p, s, e0, e1);
-  if (epi == EPI_RESID) return launch_nt<float, EPI_RESID>(nt, mt, grid, threads, p, s, e0, e1);
-  if (epi == EPI_QKV) return launch_nt<float, EPI_QKV>(nt, mt, grid, threads, p, s, e0, e1);
-  if (epi == EPI_PART) return launch_nt<float, EPI_PART>(nt, mt, grid, threads, p, s, e0, e1);
-  return launch_nt<float, EPI_SWIGLU>(nt, mt, grid, threads, p, s, e0, e1);
+  if (epi == EPI_STORE) return launch_nt<float, EPI_STORE>(nt, mt, grid, threads, q, s, e0, e1);
+  if (epi == EPI_RESID) return launch_nt<float, EPI_RESID>(nt, mt, grid, threads, q, s, e0, e1);
+  if (epi == EPI_QKV) return launch_nt<float, EPI_QKV>(nt, mt, grid, threads, q, s, e0, e1);
+  if (epi == EPI_PART) return launch_nt<float, EPI_PART>(nt, mt, grid, threads, q, s, e0, e1);
+  return launch_nt<float, EPI_SWIGLU>(nt, mt, grid, threads, q, s, e0, e1);
 }
 
 }  // namespace sd

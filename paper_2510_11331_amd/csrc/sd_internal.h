@@ -146,6 +146,7 @@ struct GemmParams {
   int ldo;
   void* out_t;        // SWIGLU: out_t[M, N/2] in the MFMA-tile layout
   RopeParams rope;    // QKV: rotary embedding of q and k, K/V appended to the cache
+  int mblocks;        // > 1: 1-D grid of (column tile, M block) pairs, XCD-aware (see gemm.hip)
 };
 
 struct AttnParams {
