@@ -83,6 +83,57 @@ template <bool NT> __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_r
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, NT ? 2 : 0));
 }
 
+// QKV projection epilogue, shared by both GEMM kernels.  Output columns are
+// the fused [q heads | k heads | v heads] rows of the weight, q and k in
+// rotary pair order: column r16 < 8 of a 16-column tile of a q or k head is
+// dim 8 b + r16 of the head, column r16 + 8 its partner dim hd/2 + 8 b + r16,
+// so the two halves of a pair meet in one lane exchange (r16 ^ 8).
+// qkv_column classifies column c0 + r16 of this lane once per tile: kind (0
+// q, 1 k, 2 v), the q column, the rotary frequency index f, and the K/V
+// element offset of (token 0, block 0); a row adds its block and token.
+template <typename T>
+__device__ __forceinline__ void qkv_column(const RopeParams& rp, int c0, int r16, int& kind, int& qcol, int& f,
+                                           size_t& kvb) {
+  const int hd = rp.hd, half = hd / 2, Nq = rp.H * hd, Nqk = Nq + rp.KV * hd;
+  kind = c0 < Nq ? 0 : c0 < Nqk ? 1 : 2;
+  qcol = 0;
+  f = 0;
+  kvb = 0;
+  if (c0 < Nqk) {
+    const int h = c0 / hd;
+    f = 8 * ((c0 % hd) / 16) + (r16 & 7);
+    const int d = r16 < 8 ? f : f + half;
+    if (h < rp.H) qcol = h * hd + d;
+    else kvb = kv_tile_off(h - rp.H, 0, 0, rp.nblk, hd) + kv_key_off<T>(0, d, hd);
+  } else {
+    const int cv = c0 + r16 - Nqk;
+    kvb = kv_tile_off(cv / hd, 0, 1, rp.nblk, hd) + kv_val_off<T>(0, cv % hd, hd);
+  }
+}
+
+// Rotary embedding of row m (position pos, KV block blk or -1) for the NT
+// tiles of a lane: o = this lane's projection, pr = its pair partner's, cs =
+// (cos, sin) of the lane's frequency; q goes to rp.q (fp32), k and v are
+// appended to the cache (skipped when blk < 0: over capacity, flagged).
+template <typename T, int NT>
+__device__ __forceinline__ void qkv_store(const RopeParams& rp, int m, int pos, int blk, int r16, const float (&o)[NT],
+                                          const float (&pr)[NT], const float2 (&cs)[NT], const int (&kind)[NT],
+                                          const int (&qcol)[NT], const size_t (&kvb)[NT]) {
+  const int off = pos & 15;
+  T* kv = (T*)rp.kv;
+  const size_t brow = (size_t)max(blk, 0) * 32 * rp.hd;   // block offset inside a head's run
+  const size_t Nq = (size_t)rp.H * rp.hd;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const float a = r16 < 8 ? o[j] : pr[j], b = r16 < 8 ? pr[j] : o[j];
+    const float y = r16 < 8 ? a * cs[j].x - b * cs[j].y : a * cs[j].y + b * cs[j].x;
+    if (kind[j] == 0) rp.q[(size_t)m * Nq + qcol[j]] = y;
+    else if (blk < 0) continue;
+    else if (kind[j] == 1) Store<T>::store(kv, kvb[j] + brow + kv_key_off<T>(off, 0, rp.hd), y);
+    else Store<T>::store(kv, kvb[j] + brow + kv_val_off<T>(off, 0, rp.hd), o[j]);
+  }
+}
+
 // Both operands are in the MFMA-tile layout (Tile<T>): fragment (tile t,
 // k-step s) of a lane is the 16-byte unit 64 (t * ksteps + s) + lane, so a
 // wave's load of one fragment is a contiguous 1 KB block.  The k-steps of a
@@ -184,16 +235,19 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     compute.template operator()<1>();
   }
 
+  // QKV: what column n0 + 16 j + r16 of this lane is (independent of the row)
+  int qkind[EPI == EPI_QKV ? NT : 1], qcol[EPI == EPI_QKV ? NT : 1], qf[EPI == EPI_QKV ? NT : 1];
+  size_t qkvb[EPI == EPI_QKV ? NT : 1];
   float2 qcs[EPI == EPI_QKV ? MT : 1][NT];
   if constexpr (EPI == EPI_QKV) {
     const int half = p.rope.hd / 2;
 #pragma unroll
+    for (int j = 0; j < NT; ++j) qkv_column<T>(p.rope, n0 + 16 * j, r16, qkind[j], qcol[j], qf[j], qkvb[j]);
+#pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        const int c0 = n0 + 16 * j, f = 8 * ((c0 % p.rope.hd) / 16) + (r16 & 7);
-        qcs[i][j] = qpos[i] >= 0 ? p.rope.tab[(size_t)qpos[i] * half + f] : float2{1.f, 0.f};
-      }
+      for (int j = 0; j < NT; ++j)
+        qcs[i][j] = qpos[i] >= 0 && qkind[j] < 2 ? p.rope.tab[(size_t)qpos[i] * half + qf[j]] : float2{1.f, 0.f};
   }
 
   // Reduction over the KW wave partials, in a fixed order: waves 4.. fold
@@ -242,35 +296,6 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     }
   }
 
-  // QKV: what column n0 + 16 j + r16 of this lane is, independent of the
-  // row: kind (0 q, 1 k, 2 v), q column, and the K/V element offset of
-  // (token 0, block 0) in the cache; a row adds its block and token offsets
-  int qkind[EPI == EPI_QKV ? NT : 1], qcol[EPI == EPI_QKV ? NT : 1];
-  size_t qkvb[EPI == EPI_QKV ? NT : 1];
-  const int Nq = p.rope.H * p.rope.hd;
-  if constexpr (EPI == EPI_QKV) {
-    const RopeParams& rp = p.rope;
-    const int hd = rp.hd, half = hd / 2, Nqk = Nq + rp.KV * hd;
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int c0 = n0 + 16 * j;             // first column of the tile
-      qkind[j] = c0 < Nq ? 0 : c0 < Nqk ? 1 : 2;
-      qcol[j] = 0;
-      qkvb[j] = 0;
-      if (c0 < Nqk) {
-        // rotary pair order: column r16 < 8 of the tile is dim 8b + r16 of
-        // head h, column r16 + 8 its partner dim hd/2 + 8b + r16
-        const int h = c0 / hd, f = 8 * ((c0 % hd) / 16) + (r16 & 7);
-        const int d = r16 < 8 ? f : f + half;
-        if (h < rp.H) qcol[j] = h * hd + d;
-        else qkvb[j] = kv_tile_off(h - rp.H, 0, 0, rp.nblk, hd) + kv_key_off<T>(0, d, hd);
-      } else {
-        const int cv = c0 + r16 - Nqk;
-        qkvb[j] = kv_tile_off(cv / hd, 0, 1, rp.nblk, hd) + kv_val_off<T>(0, cv % hd, hd);
-      }
-    }
-  }
-
   // output element (i, j, v) is row m0 + 16 i + 4 g + v, column n0 + 16 j + r16
 #pragma unroll
   for (int i = 0; i < MT; ++i)
@@ -294,29 +319,8 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
       }
       if (m >= p.M) continue;
       if constexpr (EPI == EPI_QKV) {
-        const int pos = qpos[i];                // this lane's row m (v == wave)
-        if (pos < 0) continue;                  // row without an input (no pending draft token)
-        const int blk = qblk[i];                // -1: K/V not written (over capacity, flagged)
-        const int off = pos & 15;
-        T* kv = (T*)p.rope.kv;
-        const size_t brow = (size_t)max(blk, 0) * 32 * p.rope.hd;   // block offset inside a head's run
-#pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          if (qkind[j] == 0) {
-            const float2 cs = qcs[i][j];
-            const float a = r16 < 8 ? o[j] : pr[j], b = r16 < 8 ? pr[j] : o[j];
-            p.rope.q[(size_t)m * Nq + qcol[j]] = r16 < 8 ? a * cs.x - b * cs.y : a * cs.y + b * cs.x;
-          } else if (qkind[j] == 1) {
-            if (blk < 0) continue;
-            const float2 cs = qcs[i][j];
-            const float a = r16 < 8 ? o[j] : pr[j], b = r16 < 8 ? pr[j] : o[j];
-            Store<T>::store(kv, qkvb[j] + brow + kv_key_off<T>(off, 0, p.rope.hd),
-                            r16 < 8 ? a * cs.x - b * cs.y : a * cs.y + b * cs.x);
-          } else {
-            if (blk < 0) continue;
-            Store<T>::store(kv, qkvb[j] + brow + kv_val_off<T>(off, 0, p.rope.hd), o[j]);
-          }
-        }
+        if (qpos[i] < 0) continue;              // row without an input (no pending draft token)
+        qkv_store<T, NT>(p.rope, m, qpos[i], qblk[i], r16, o, pr, qcs[i], qkind, qcol, qkvb);
       } else if constexpr (EPI == EPI_SWIGLU) {
         // tiles (2k, 2k+1) are the gate and up rows of the same 16 outputs
         const int F = p.N / 2;
@@ -333,6 +337,193 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
         }
       }
     }
+}
+
+// Row-tiled GEMM for passes with more than one 64-row block (batched
+// verify at B >= 32, prefill): there every weight byte meets hundreds of
+// rows, so the operands are staged once per workgroup in LDS and shared.
+// A workgroup of 4 waves (2 x 2) owns a BM x BN = 32 MF x 32 NF output tile;
+// wave (wm, wn) owns the 16 MF x 16 NF sub-tile at (wm 16 MF, wn 16 NF).
+// K advances in stages of two k-steps (64 bf16): the 2 (BM + BN) / 16 1 KB
+// fragments of a stage are loaded by the 4 waves into registers while the
+// previous stage is multiplied out of LDS, then written to the other LDS
+// buffer (one barrier per stage).  Rows at or past M load zeros (range-
+// checked buffer loads).  Tile order: the row tiles of one column tile take
+// consecutive slots of one XCD (1-D grid, round-robin dispatch over 8 XCDs),
+// so its weights are fetched from HBM once and re-read from that XCD's L2.
+template <int MF, int NF, int EPI>
+__global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
+  using T = bf16_t;
+  constexpr int BM = 32 * MF, BN = 32 * NF;
+  constexpr int FA = 2 * BM / 16, FW = 2 * BN / 16;   // fragments per stage
+  extern __shared__ __align__(16) unsigned char smem[];
+  u32x4* lds = (u32x4*)smem;                          // [2][FA + FW][64]
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int ksteps = p.K * 2 / 64, stages = ksteps / 2;
+  const int gx = p.N / BN, gz = (p.M + BM - 1) / BM;
+  int bx, bz;
+  {
+    const int w = blockIdx.x;
+    if (gx % 8 == 0) {
+      const int j = w >> 3;
+      bz = j % gz;
+      bx = (j / gz) * 8 + (w & 7);
+    } else {
+      bx = w % gx;
+      bz = w / gx;
+    }
+  }
+  const uint32_t tile_bytes = (uint32_t)ksteps * 1024u;
+  const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)p.W + (size_t)bx * (BN / 16) * tile_bytes, (BN / 16) * tile_bytes);
+  const __amdgpu_buffer_rsrc_t ar = buf_rsrc((const char*)p.A + (size_t)bz * (BM / 16) * tile_bytes, (BM / 16) * tile_bytes);
+  const int mvalid = p.M - bz * BM;                   // rows of this tile below M
+
+  // this wave's share of a stage: A fragments f = 4 k + wave (k < MF), W
+  // fragments f = 4 k + wave (k < NF); fragment f = 2 t + u is (16-row tile
+  // t, k-step u of the stage)
+  u32x4 ra[MF], rw[NF];
+  auto gload = [&](int st) {
+#pragma unroll
+    for (int k = 0; k < MF; ++k) {
+      const int f = 4 * k + wave, t = f >> 1, u = f & 1;
+      const uint32_t off = 16 * t + r16 < mvalid ? ((uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u)
+                                                 : OOB;
+      ra[k] = buf_load16<false>(ar, off);
+    }
+#pragma unroll
+    for (int k = 0; k < NF; ++k) {
+      const int f = 4 * k + wave, t = f >> 1, u = f & 1;
+      rw[k] = buf_load16<false>(wr, (uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u);
+    }
+  };
+  auto lwrite = [&](int buf) {
+    u32x4* base = lds + (size_t)buf * (FA + FW) * 64;
+#pragma unroll
+    for (int k = 0; k < MF; ++k) base[(4 * k + wave) * 64 + lane] = ra[k];
+#pragma unroll
+    for (int k = 0; k < NF; ++k) base[(FA + 4 * k + wave) * 64 + lane] = rw[k];
+  };
+
+  f32x4 acc[MF][NF];
+#pragma unroll
+  for (int i = 0; i < MF; ++i)
+#pragma unroll
+    for (int j = 0; j < NF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  gload(0);
+  lwrite(0);
+  __syncthreads();
+  for (int st = 0; st < stages; ++st) {
+    if (st + 1 < stages) gload(st + 1);
+    const u32x4* base = lds + (size_t)(st & 1) * (FA + FW) * 64;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      u32x4 a[MF], b[NF];
+#pragma unroll
+      for (int i = 0; i < MF; ++i) a[i] = base[(2 * (wm * MF + i) + u) * 64 + lane];
+#pragma unroll
+      for (int j = 0; j < NF; ++j) b[j] = base[(FA + 2 * (wn * NF + j) + u) * 64 + lane];
+#pragma unroll
+      for (int i = 0; i < MF; ++i)
+#pragma unroll
+        for (int j = 0; j < NF; ++j) acc[i][j] = Mfma<T>::step(a[i], b[j], acc[i][j]);
+    }
+    if (st + 1 < stages) lwrite((st + 1) & 1);
+    __syncthreads();
+  }
+
+  // epilogue: element (i, j, v) is row bz BM + wm 16 MF + 16 i + 4 g + v,
+  // column n0 + 16 j + r16 with n0 the first column of the wave's sub-tile
+  const int n0 = bx * BN + wn * 16 * NF;
+  int qkind[EPI == EPI_QKV ? NF : 1], qcol[EPI == EPI_QKV ? NF : 1], qf[EPI == EPI_QKV ? NF : 1];
+  size_t qkvb[EPI == EPI_QKV ? NF : 1];
+  if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+    for (int j = 0; j < NF; ++j) qkv_column<T>(p.rope, n0 + 16 * j, r16, qkind[j], qcol[j], qf[j], qkvb[j]);
+  }
+#pragma unroll
+  for (int i = 0; i < MF; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int m = bz * BM + wm * 16 * MF + 16 * i + 4 * g + v;
+      float o[NF], pr[EPI == EPI_QKV ? NF : 1];
+#pragma unroll
+      for (int j = 0; j < NF; ++j) o[j] = acc[i][j][v];
+      if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+        for (int j = 0; j < NF; ++j) pr[j] = __shfl_xor(o[j], 8);
+      }
+      if (m >= p.M) continue;
+      if constexpr (EPI == EPI_QKV) {
+        const int pos = p.rope.row_pos[m];
+        if (pos < 0) continue;
+        const int blk = p.rope.row_blk[m];
+        const int half = p.rope.hd / 2;
+        float2 cs[NF];
+#pragma unroll
+        for (int j = 0; j < NF; ++j) cs[j] = qkind[j] < 2 ? p.rope.tab[(size_t)pos * half + qf[j]] : float2{1.f, 0.f};
+        qkv_store<T, NF>(p.rope, m, pos, blk, r16, o, pr, cs, qkind, qcol, qkvb);
+      } else if constexpr (EPI == EPI_SWIGLU) {
+        const int F = p.N / 2;
+#pragma unroll
+        for (int j = 0; j < NF; j += 2)
+          Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F), silu(o[j]) * o[j + 1]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < NF; ++j) {
+          float* dst = p.out + (size_t)m * p.ldo + n0 + 16 * j + r16;
+          if constexpr (EPI == EPI_RESID) *dst += o[j];
+          else *dst = o[j];
+        }
+      }
+    }
+}
+
+size_t gemm_rows_lds(int mf, int nf) { return (size_t)2 * (2 * 32 * mf / 16 + 2 * 32 * nf / 16) * 1024; }
+
+template <int EPI, int MF, int NF>
+static hipError_t launch_rows_t(int gz, const GemmParams& p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const size_t lds = gemm_rows_lds(MF, NF);
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_rows_kernel<MF, NF, EPI>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  launch_k(gemm_rows_kernel<MF, NF, EPI>, dim3(p.N / (32 * NF) * gz), dim3(256), (uint32_t)lds, s, e0, e1, p);
+  return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t launch_rows_e(int mf, int nf, int gz, const GemmParams& p, hipStream_t s, hipEvent_t e0,
+                                hipEvent_t e1) {
+#define SD_ROWS_CASE(MFv, NFv) \
+  if (mf == MFv && nf == NFv) return launch_rows_t<EPI, MFv, NFv>(gz, p, s, e0, e1);
+  SD_ROWS_CASE(4, 2) SD_ROWS_CASE(5, 2) SD_ROWS_CASE(6, 2) SD_ROWS_CASE(8, 2)
+  SD_ROWS_CASE(4, 4) SD_ROWS_CASE(5, 4) SD_ROWS_CASE(6, 4) SD_ROWS_CASE(8, 4)
+#undef SD_ROWS_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_rows(int epi, int mf, int nf, const GemmParams& p, hipStream_t s, hipEvent_t e0,
+                            hipEvent_t e1) {
+  const int bn = 32 * nf, bm = 32 * mf;
+  if (p.N % bn || p.M < 1 || ((size_t)p.K * 2) % GEMM_CHUNK) return hipErrorInvalidValue;
+  const int gz = (p.M + bm - 1) / bm;
+  switch (epi) {
+    case EPI_STORE: return launch_rows_e<EPI_STORE>(mf, nf, gz, p, s, e0, e1);
+    case EPI_RESID: return launch_rows_e<EPI_RESID>(mf, nf, gz, p, s, e0, e1);
+    case EPI_SWIGLU: return launch_rows_e<EPI_SWIGLU>(mf, nf, gz, p, s, e0, e1);
+    case EPI_QKV:
+      if (p.rope.hd % 16 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd) return hipErrorInvalidValue;
+      return launch_rows_e<EPI_QKV>(mf, nf, gz, p, s, e0, e1);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 // row-major [N, K] -> MFMA-tile layout, one 16-byte unit per thread

@@ -223,6 +223,11 @@ inline void launch_k(K kern, dim3 grid, dim3 block, uint32_t shm, hipStream_t s,
 }
 
 int gemm_max_waves(int mt, int nt);   // waves per workgroup the (mt, nt) tile allows
+// Row-tiled bf16 GEMM for passes of several 64-row blocks: 32 mf x 32 nf
+// output tiles, mf in {4, 5, 6, 8}, nf in {2, 4}; epi: STORE, RESID, SWIGLU
+// or QKV (no K split).  N must be a multiple of 32 nf.
+hipError_t launch_gemm_rows(int epi, int mf, int nf, const GemmParams& p, hipStream_t s, hipEvent_t e0 = nullptr,
+                            hipEvent_t e1 = nullptr);
 hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
                        const GemmParams& p, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // tab[pos * half + i] = (cos, sin) of pos * theta^(-i/half), pos < n_pos, i < half
