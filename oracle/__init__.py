@@ -19,9 +19,12 @@ Modules
   sd        the draft -> verify -> accept -> rollback loop and plain
             autoregressive decoding.
   exact     exact laws of the implemented sampling rules (for pins).
+  sched     the serving scheduler's cost and latency model, the batching
+            dynamic program and the speculation-length search, and the
+            closed-form uplink allocation.
 
 Parity pins: every function here is pinned by ``tests/test_oracle_*.py``
 against closed forms, library routines (torch CPU), brute force or the
 distribution-preservation property of speculative sampling.
 """
-from . import model, sampling, sd, exact  # noqa: F401
+from . import model, sampling, sd, exact, sched  # noqa: F401
