@@ -16,11 +16,11 @@ SD_DTYPE_BF16, SD_DTYPE_F32 = 0, 1
 (SD_PROF_GEMM_VERIFY_GATEUP, SD_PROF_GEMM_VERIFY_ALL, SD_PROF_ATTN_VERIFY,
  SD_PROF_VERIFY, SD_PROF_DRAFT) = range(5)
 
-# the symbols include/sd.h declares (checked by the CPU test suite)
+# the symbols include/sd.h and include/sd_sched.h declare (checked by the CPU test suite)
 EXPORTS = ("sd_kv_pool_bytes", "sd_workspace_bytes", "sd_init", "sd_prefill", "sd_release",
            "sd_draft_step", "sd_verify", "sd_accept_resample", "sd_kv_commit", "sd_slot_state",
            "sd_check", "sd_profile", "sd_profile_read", "sd_destroy", "sd_strerror", "sd_last_error",
-           "sd_pack_linear")
+           "sd_pack_linear", "sd_sched_latency", "sd_sched_batching", "sd_sched_plan", "sd_sched_uplink")
 
 
 class ModelCfg(C.Structure):
@@ -44,6 +44,16 @@ class Config(C.Structure):
                 ("prefill_rows", C.c_int), ("temperature", C.c_float), ("greedy", C.c_int),
                 ("kv_pool_target", C.c_void_p), ("kv_pool_draft", C.c_void_p),
                 ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t)]
+
+
+class SchedModel(C.Structure):
+    _fields_ = [("n_layers", C.c_int), ("d_model", C.c_int), ("d_ffn", C.c_int)]
+
+
+class SchedCfg(C.Structure):
+    _fields_ = [("draft", SchedModel), ("target", SchedModel), ("c1_draft", C.c_double),
+                ("c2_draft", C.c_double), ("c1_verify", C.c_double), ("c2_verify", C.c_double),
+                ("alpha", C.c_double), ("o_max", C.c_int), ("mem_budget", C.c_double)]
 
 
 class SDError(RuntimeError):
@@ -91,6 +101,14 @@ def lib():
         "sd_strerror": (C.c_char_p, [I]),
         "sd_last_error": (C.c_char_p, []),
         "sd_pack_linear": (I, [P, P, I, I, I, P]),
+        "sd_sched_latency": (I, [C.POINTER(SchedCfg), I, C.POINTER(C.c_int32), I, C.POINTER(C.c_int32), I,
+                                 C.POINTER(C.c_double)]),
+        "sd_sched_batching": (I, [C.POINTER(SchedCfg), I, C.POINTER(C.c_int32), I, C.POINTER(C.c_int32),
+                                  C.POINTER(I), C.POINTER(C.c_double)]),
+        "sd_sched_plan": (I, [C.POINTER(SchedCfg), I, C.POINTER(C.c_int32), I, C.POINTER(C.c_int32),
+                              C.POINTER(I), C.POINTER(I), C.POINTER(C.c_double), C.POINTER(C.c_double)]),
+        "sd_sched_uplink": (I, [I, C.POINTER(C.c_int32), C.POINTER(C.c_double), C.c_double, C.c_double,
+                                C.POINTER(C.c_double), C.POINTER(C.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)

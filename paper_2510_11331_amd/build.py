@@ -1,7 +1,8 @@
 """Build libsd.so (HIP kernels + C ABI) for gfx950, in-tree.
 
-Every .hip file under csrc/ is compiled by hipcc for gfx950 and the objects
-are linked into paper_2510_11331_amd/libsd.so.  The HIP runtime is recorded
+Every .hip file under csrc/ is compiled by hipcc for gfx950, every .cpp file
+(host-only code: the serving scheduler) by g++, and the objects are linked
+into paper_2510_11331_amd/libsd.so.  The HIP runtime is recorded
 as the unversioned ``libamdhip64.so`` (the name PyTorch-ROCm loads from its
 own lib directory), so a process that already runs torch shares one HIP
 runtime with libsd; outside such a process the rpath finds ROCm's copy.
@@ -29,6 +30,9 @@ HIPCC_FLAGS = [
     "-Wno-unused-command-line-argument",
     "-I", INCLUDE, "-I", CSRC,
 ]
+
+
+GXX_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-I", INCLUDE, "-I", CSRC]
 
 
 def _hip_runtime_dir() -> str:
@@ -59,12 +63,17 @@ def _run(cmd, verbose):
 def build(verbose: bool = False, jobs: int = 8) -> str:
     hipcc = shutil.which("hipcc") or os.path.join(ROCM, "bin", "hipcc")
     os.makedirs(BUILD_DIR, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
-    objs = [os.path.join(BUILD_DIR, os.path.basename(s)[:-4] + ".o") for s in srcs]
+    # HIP sources (kernels + host runtime) with hipcc; host-only C++ (the
+    # serving scheduler) with g++
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
+    objs = [os.path.join(BUILD_DIR, os.path.splitext(os.path.basename(s))[0] + ".o") for s in srcs]
 
     def compile_one(so):
         s, o = so
-        _run([hipcc, *HIPCC_FLAGS, "-c", s, "-o", o], verbose)
+        if s.endswith(".cpp"):
+            _run(["g++", *GXX_FLAGS, "-c", s, "-o", o], verbose)
+        else:
+            _run([hipcc, *HIPCC_FLAGS, "-c", s, "-o", o], verbose)
 
     with ThreadPoolExecutor(max_workers=max(1, min(jobs, len(srcs)))) as ex:
         list(ex.map(compile_one, zip(srcs, objs)))

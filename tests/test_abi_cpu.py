@@ -16,9 +16,12 @@ pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libsd.so not bu
 
 
 def header_functions():
-    src = open(os.path.join(ROOT, "include", "sd.h")).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(sd_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in ("sd.h", "sd_sched.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names |= set(re.findall(r"\b(sd_[a-z_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_exports_every_declared_function():
@@ -54,7 +57,7 @@ def test_sizes_and_validation():
     assert L.sd_kv_pool_bytes(C.byref(c), 0) == t.n_layers * 32 * 2 * t.n_kv_heads * 16 * t.head_dim * 4
     assert L.sd_workspace_bytes(C.byref(c)) > 0
     bad = [dict(kv_block=8), dict(gamma_max=0), dict(gamma_max=17), dict(max_batch=5),
-           dict(temperature=0.0), dict(prefill_rows=0), dict(max_ctx=1)]
+           dict(temperature=0.0), dict(prefill_rows=0), dict(max_ctx=1), dict(max_ctx=32769)]
     for kw in bad:
         cb = make_cfg(**kw)
         assert L.sd_workspace_bytes(C.byref(cb)) == 0, kw
