@@ -47,6 +47,13 @@ def parse():
     ap.add_argument("--trace-summary", metavar="KERNEL_TRACE_CSV",
                     help="summarise a rocprofv3 --kernel-trace csv of a default bench run (whole run by kernel, "
                          "and the median timed step by kernel and launch shape) as markdown and exit")
+    ap.add_argument("--fit-runtime", metavar="OUT_JSON",
+                    help="fit the runtime model T(b, F) = c1 F b + c2 of the verify and draft forwards of the "
+                         "7B-shape pair on this GPU (graph-replayed passes over batch sizes, contexts and "
+                         "speculation lengths), write the fit to OUT_JSON and exit")
+    ap.add_argument("--schedule", metavar="FIT_JSON",
+                    help="with a runtime fit: plan batches and speculation length for synthetic task sets, "
+                         "compare with the baseline policies (predicted), and run plans on the GPU (measured)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc counter_collection.csv files of --pmc-pass runs "
                          "(FETCH_SIZE, then WRITE_SIZE) into profiles/pmc_traffic.json and exit")
@@ -241,6 +248,202 @@ def trace_summary(path: str, warmup: int, steps: int) -> None:
         print(f"| `{n}` | {len(v)} | {sum(v):.1f} | {np.mean(v):.2f} | {np.median(v):.2f} |")
 
 
+def paper_flops_verify(J, h1, h2, kv, l):
+    """Per-task FLOPs of a verify forward of 1 + l tokens over kv cached
+    tokens (the decoding-stage form of eq. flops_v)."""
+    return 4.0 * J * h1 * (1.0 + l) * (2.0 * h1 + kv + l + 1.0 + h2)
+
+
+def paper_flops_draft(J, h1, h2, kv):
+    """Per-task FLOPs of one draft decode forward over kv cached tokens (eq. flops_d, decoding stage)."""
+    return 4.0 * J * h1 * (2.0 * h1 + kv + 1.0 + h2)
+
+
+def linear_fit(x, y):
+    """Least squares y = c1 x + c2; returns c1, c2, R^2, max relative residual."""
+    x, y = np.asarray(x, dtype=np.float64), np.asarray(y, dtype=np.float64)
+    A = np.stack([x, np.ones_like(x)], axis=1)
+    (c1, c2), *_ = np.linalg.lstsq(A, y, rcond=None)
+    pred = c1 * x + c2
+    r2 = 1.0 - float(np.sum((y - pred) ** 2) / np.sum((y - y.mean()) ** 2))
+    return float(c1), float(c2), r2, float(np.max(np.abs(pred - y) / y))
+
+
+def replay_ms(graph, n):
+    import torch
+    graph.replay()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record()
+    for k in range(n):
+        graph.replay()
+        ev[k + 1].record()
+    torch.cuda.synchronize()
+    return float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(n)]))
+
+
+def fit_runtime(out_json: str) -> None:
+    """Runtime model of the paper's serving scheduler refit on this GPU: the
+    verify pass of the 7B-shape target and one decode forward of its draft,
+    each captured as a HIP graph and replayed, over batch sizes b, cached
+    contexts and speculation lengths l; F from the paper's FLOPs formulas."""
+    import torch
+    from paper_2510_11331_amd import SDEngine
+    from paper_2510_11331_amd.engine import uniforms_device
+
+    wl = synth.WORKLOADS["7b_b8"]
+    t, d = wl.target, wl.draft
+    ctxs, bs, ls = [256, 1024, 2048], [1, 4, 8, 16, 32], [1, 2, 4, 8]
+    tg, dg = synth.StreamingWeights(t, 1), synth.StreamingWeights(d, 2)
+    eng = SDEngine(t, d, tg, dg, max_slots=32, max_batch=32, gamma_max=8, max_ctx=max(ctxs) + 64,
+                   prefill_rows=2048, temperature=1.0)
+    tg.close(); dg.close()
+    rows = []
+    for ctx in ctxs:
+        prompts = synth.prompts(32, [ctx] * 32, t.vocab)
+        eng.prefill(list(range(32)), prompts, [32] * 32)
+        for b in bs:
+            u = uniforms_device(synth.uniform_table(42, list(range(b)), 1, 8)[0])
+            bd = eng.batch(list(range(b)), 2)
+            gd = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gd):
+                eng.draft_step(bd, 1, u)
+            td = replay_ms(gd, 10)
+            del gd
+            for l in ls:
+                bv = eng.batch(list(range(b)), l)
+                gv = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gv):
+                    eng.verify(bv)
+                tv = replay_ms(gv, 10)
+                del gv
+                rows.append({"ctx": ctx, "b": b, "l": l, "verify_ms": tv, "draft_ms": td})
+                print(f"[fit] ctx {ctx} b {b} l {l}: verify {tv:.3f} ms, draft forward {td:.3f} ms",
+                      file=sys.stderr, flush=True)
+        for s in range(32):
+            eng.release(s)
+    eng.close()
+    # P = ctx - 1 positions are cached after the prefill of prompt[:-1]
+    xv = [paper_flops_verify(t.n_layers, t.d_model, t.d_ffn, r["ctx"] - 1, r["l"]) * r["b"] for r in rows]
+    yv = [r["verify_ms"] * 1e-3 for r in rows]
+    dr = [r for r in rows if r["l"] == 1]
+    xd = [paper_flops_draft(d.n_layers, d.d_model, d.d_ffn, r["ctx"]) * r["b"] for r in dr]
+    yd = [r["draft_ms"] * 1e-3 for r in dr]
+    c1v, c2v, r2v, ev = linear_fit(xv, yv)
+    c1d, c2d, r2d, ed = linear_fit(xd, yd)
+    out = {"what": "T(b, F) = c1 F b + c2 (seconds) refit on one MI355X: 7B-shape bf16 target verify pass, "
+                   "2-layer d1024 draft decode forward; graph replay; F from the paper's FLOPs formulas",
+           "target": [t.n_layers, t.d_model, t.d_ffn], "draft": [d.n_layers, d.d_model, d.d_ffn],
+           "c_verify": [c1v, c2v], "c_draft": [c1d, c2d],
+           "fit_quality": {"verify_r2": r2v, "verify_max_rel_residual": ev, "draft_r2": r2d,
+                           "draft_max_rel_residual": ed},
+           "paper_table2": {"c_verify": [2.08e-14, 1.28e-2], "c_draft": [4.11e-13, 0.56e-3],
+                            "hardware": "RTX 4500 (verify), RTX 3080 (draft)"},
+           "points": rows}
+    with open(out_json, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps({k: out[k] for k in ("c_verify", "c_draft", "fit_quality")}), flush=True)
+
+
+def schedule_eval(fit_json: str) -> None:
+    """The paper's scheduler (libsd sd_sched_*) with the runtime model refit on
+    this GPU.  Predicted: the Section V task set (100 tasks, input lengths
+    uniform in [1, 512], every task given 2048 output tokens, acceptance rate
+    0.8, speculation length up to 10, 16 GB draft memory) under the proposed
+    plan (Algorithm 1 + the best speculation length) and the baseline
+    policies of the paper, with this GPU's coefficients and with the
+    paper's.  Measured: a 16-task ragged set run by the two-stream pipeline
+    for each plan; the decode steps are timed and compared with the model's
+    decode-step latency (the paper's first step also holds the prefill, which
+    runs separately here)."""
+    import torch
+    from paper_2510_11331_amd import SDEngine, sched, generate
+
+    fit = json.load(open(fit_json))
+    base = {"draft": fit["draft"], "target": fit["target"]}
+    ours = dict(base, c_draft=fit["c_draft"], c_verify=fit["c_verify"])
+    paper = dict(base, c_draft=fit["paper_table2"]["c_draft"], c_verify=fit["paper_table2"]["c_verify"])
+
+    def chunks(order, size):
+        return [order[i:i + size] for i in range(0, len(order), size)]
+
+    def best_over_l(cfg, lengths, batches, l_max):
+        ts = [sched.latency(cfg, lengths, batches, l) for l in range(1, l_max + 1)]
+        return int(np.argmin(ts)) + 1, float(min(ts))
+
+    def policies(cfg, lengths, l_max):
+        order = sorted(range(len(lengths)), key=lambda k: (lengths[k], k))
+        p = sched.plan(cfg, lengths, l_max)
+        fsl_b, fsl_t = sched.batching(cfg, lengths, 7)
+        res = {"proposed (Algorithm 1 + best l)": (p["l"], len(p["batches"]), p["t_inf"]),
+               "fixed l = 7 (FSL), Algorithm 1 batching": (7, len(fsl_b), fsl_t)}
+        for name, bt in (("no batching", chunks(order, 1)), ("static batches of 8", chunks(order, 8)),
+                         ("one batch (max batching)", [order])):
+            l, t = best_over_l(cfg, lengths, bt, l_max)
+            res[name] = (l, len(bt), t)
+        # the proposed plan without the pipeline: batches one after the other
+        serial = sum(sched.latency(cfg, lengths, [b], p["l"]) for b in p["batches"])
+        res["proposed plan, no pipeline"] = (p["l"], len(p["batches"]), serial)
+        return res, p
+
+    rng = np.random.default_rng(7)
+    lengths = [int(x) for x in rng.integers(1, 513, 100)]
+    out = {"fit": {k: fit[k] for k in ("c_verify", "c_draft", "fit_quality")}, "predicted": {}}
+    for label, cfg in (("mi355x_fit", ours), ("paper_table2", paper)):
+        c = dict(cfg, alpha=0.8, o_max=2048, mem_budget=16e9)
+        res, _ = policies(c, lengths, 10)
+        out["predicted"][label] = {k: {"l": v[0], "batches": v[1], "t_inf_s": round(v[2], 4)} for k, v in res.items()}
+        print(f"[schedule] predicted, {label} coefficients:", file=sys.stderr)
+        for k, v in res.items():
+            print(f"   {k:44s} l={v[0]:2d} batches={v[1]:3d} T_inf={v[2]:9.3f} s", file=sys.stderr, flush=True)
+
+    # measured: 16 ragged tasks, random-init 7B-shape pair (acceptance ~0.45 per draft)
+    wl = synth.WORKLOADS["7b_b8"]
+    t, d = wl.target, wl.draft
+    K, alpha, o_max, l_max = 16, 0.45, 48, 8
+    rng = np.random.default_rng(11)
+    lens = [int(x) for x in rng.integers(64, 1025, K)]
+    tg, dg = synth.StreamingWeights(t, 1), synth.StreamingWeights(d, 2)
+    reserve = (o_max + 2) * (l_max + 1)           # tokens a task may emit over the steps of any plan
+    eng = SDEngine(t, d, tg, dg, max_slots=K, max_batch=K, gamma_max=l_max, max_ctx=1024 + reserve + 64,
+                   prefill_rows=2048, temperature=1.0)
+    tg.close(); dg.close()
+    prompts = synth.prompts(K, lens, t.vocab)
+    c = dict(ours, alpha=alpha, o_max=o_max)
+    p = sched.plan(c, lens, l_max)
+    order = sorted(range(K), key=lambda k: (lens[k], k))
+    l1, _ = best_over_l(c, lens, [order], l_max)
+    plans = {"proposed": (p["batches"], p["l"]), "one batch": ([order], l1),
+             "fixed l = 7": (sched.batching(c, lens, 7)[0], 7)}
+    c1 = dict(c, o_max=1)
+    measured = {}
+    for name, (batches, l) in plans.items():
+        L = (1 - alpha ** (l + 1)) / (1 - alpha)
+        N = int(np.ceil(o_max / L))
+        pred = sched.latency(c, lens, batches, l) - sched.latency(c1, lens, batches, l)
+        serial = sum(sched.latency(c, lens, [b], l) - sched.latency(c1, lens, [b], l) for b in batches)
+        eng.prefill(list(range(K)), prompts, [reserve] * K)
+        bts = [eng.batch(list(b), l) for b in batches]
+        uts = [synth.uniform_table(42, list(b), N, l) for b in batches]
+        generate(eng, bts, [u[:1] for u in uts], 1, two_streams=True)          # warm-up step
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        generate(eng, bts, [u[1:] for u in uts], N - 1, two_streams=True)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3
+        measured[name] = {"l": l, "batches": [len(b) for b in batches], "decode_steps": N - 1,
+                          "measured_ms": round(ms, 2), "predicted_ms": round(pred * 1e3, 2),
+                          "predicted_serial_ms": round(serial * 1e3, 2)}
+        print(f"[schedule] measured {name}: l={l} batches={[len(b) for b in batches]} {N - 1} decode steps: "
+              f"{ms:.1f} ms (model, two-stage pipeline {pred * 1e3:.1f} ms; serial {serial * 1e3:.1f} ms)",
+              file=sys.stderr, flush=True)
+        for s in range(K):
+            eng.release(s)
+    eng.close()
+    out["measured"] = {"tasks": K, "input_lengths": lens, "alpha": alpha, "o_max": o_max, "plans": measured}
+    print(json.dumps(out), flush=True)
+
+
 def graph_latencies(eng, batch, u_step, n):
     """Median-ready lists of n replay times (ms) of the verify pass and of the
     gamma draft calls of one batch, each captured as a HIP graph."""
@@ -275,6 +478,12 @@ def main():
         return
     if args.trace_summary:
         trace_summary(args.trace_summary, args.warmup, args.steps)
+        return
+    if args.fit_runtime:
+        fit_runtime(args.fit_runtime)
+        return
+    if args.schedule:
+        schedule_eval(args.schedule)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
