@@ -353,9 +353,10 @@ def schedule_eval(fit_json: str) -> None:
     plan (Algorithm 1 + the best speculation length) and the baseline
     policies of the paper, with this GPU's coefficients and with the
     paper's.  Measured: a 16-task ragged set run by the two-stream pipeline
-    for each plan; the decode steps are timed and compared with the model's
-    decode-step latency (the paper's first step also holds the prefill, which
-    runs separately here)."""
+    for each plan; steps 2..N are timed and compared with the model's latency
+    of the same steps.  The engine processes prompts before step 1, so plans
+    are made with the decoding-stage first step (prefill_separate), and one
+    plan with the paper's first-step prefill pricing for comparison."""
     import torch
     from paper_2510_11331_amd import SDEngine, sched, generate
 
@@ -409,12 +410,18 @@ def schedule_eval(fit_json: str) -> None:
                    prefill_rows=2048, temperature=1.0)
     tg.close(); dg.close()
     prompts = synth.prompts(K, lens, t.vocab)
-    c = dict(ours, alpha=alpha, o_max=o_max)
+    # the engine processes the prompts before the first step, so every step it
+    # runs is a decoding step: plans are made with prefill_separate, and also,
+    # for comparison, with the paper's first-step (prefill) pricing
+    c = dict(ours, alpha=alpha, o_max=o_max, prefill_separate=True)
+    c_paper = dict(c, prefill_separate=False)
     p = sched.plan(c, lens, l_max)
+    p_paper = sched.plan(c_paper, lens, l_max)
     order = sorted(range(K), key=lambda k: (lens[k], k))
     l1, _ = best_over_l(c, lens, [order], l_max)
-    plans = {"proposed": (p["batches"], p["l"]), "one batch": ([order], l1),
-             "fixed l = 7": (sched.batching(c, lens, 7)[0], 7)}
+    plans = {"proposed": (p["batches"], p["l"]),
+             "proposed, step-1 prefill pricing": (p_paper["batches"], p_paper["l"]),
+             "one batch": ([order], l1), "fixed l = 7": (sched.batching(c, lens, 7)[0], 7)}
     c1 = dict(c, o_max=1)
     measured = {}
     for name, (batches, l) in plans.items():

@@ -49,6 +49,15 @@ typedef struct {
     double alpha;                  /* acceptance rate, 0 <= alpha <= 1          */
     int o_max;                     /* output tokens given to every task, >= 1   */
     double mem_budget;             /* draft memory budget in bytes; <= 0: none  */
+    int prefill_separate;          /* 1: the prompts are processed before step
+                                      1 (as sd_prefill does), so step 1 is a
+                                      decoding-stage step like the others: the
+                                      draft forwards over one token, the verify
+                                      over 1 + l tokens, with I_m - 1 + (n-1) L
+                                      tokens cached before step n; prompt
+                                      processing is not part of T_inf.
+                                      0: the paper's first step (eqs. flops_d,
+                                      flops_v at n = 1).                        */
 } sd_sched_cfg;
 
 /* Expected inference latency T_inf (seconds) of a plan: task k (input length

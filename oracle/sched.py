@@ -41,6 +41,12 @@ implements in places):
   S-5 h1 = model width, h2 = FFN width, J = number of decoder blocks; the
       FLOPs formulas are the paper's (two FFN matrices); the fitted c1
       absorbs the constant factor of the SwiGLU FFN actually run.
+
+Option cfg["prefill_separate"] (an engine that processes the prompts before
+the first step, as the HIP path does): step 1 is a decoding-stage step like
+the others, with the draft's first forward over one token and the verify
+over 1 + l tokens, I_m - 1 tokens cached (the prompt minus the token the
+step starts from); the prompt processing is not part of T_inf.
 """
 from __future__ import annotations
 
@@ -86,12 +92,32 @@ def runtime(c: Tuple[float, float], F: float, b: int) -> float:
     return c[0] * F * b + c[1]
 
 
+def flops_draft_decode(J: int, h1: int, h2: int, kv: float) -> float:
+    """FLOPs of one draft forward of one token over kv cached tokens (the
+    decoding-stage form of eq. flops_d)."""
+    return 4.0 * J * h1 * (2.0 * h1 + kv + 1.0 + h2)
+
+
+def flops_verify_decode(J: int, h1: int, h2: int, kv: float, l: int) -> float:
+    """FLOPs of one verify forward of 1 + l tokens over kv cached tokens (the
+    decoding-stage form of eq. flops_v)."""
+    return 4.0 * J * h1 * (1.0 + l) * (2.0 * h1 + kv + l + 1.0 + h2)
+
+
 def step_times(cfg: Dict, b: int, I_m: float, l: int, n: int, L: float) -> Tuple[float, float]:
     """(T^d_{n,m}, T^v_{n,m}) of a batch of b tasks with input length I_m
     (eq. d_latency, eq. v_latency)."""
     Jd, h1d, h2d = cfg["draft"]
     Jv, h1v, h2v = cfg["target"]
     td = 0.0
+    if cfg.get("prefill_separate"):
+        # every step is a decoding step; before step n the caches hold the
+        # prompt minus one token plus (n - 1) L emitted tokens
+        base = I_m - 1.0 + (n - 1) * L
+        for i in range(1, l + 1):
+            td += runtime(cfg["c_draft"], flops_draft_decode(Jd, h1d, h2d, base + i - 1), b)
+        tv = runtime(cfg["c_verify"], flops_verify_decode(Jv, h1v, h2v, base, l), b)
+        return td, tv
     for i in range(1, l + 1):
         td += runtime(cfg["c_draft"], flops_draft(Jd, h1d, h2d, I_m, i, n, L), b)
     tv = runtime(cfg["c_verify"], flops_verify(Jv, h1v, h2v, I_m, l, n, L), b)

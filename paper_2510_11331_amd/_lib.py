@@ -53,7 +53,8 @@ class SchedModel(C.Structure):
 class SchedCfg(C.Structure):
     _fields_ = [("draft", SchedModel), ("target", SchedModel), ("c1_draft", C.c_double),
                 ("c2_draft", C.c_double), ("c1_verify", C.c_double), ("c2_verify", C.c_double),
-                ("alpha", C.c_double), ("o_max", C.c_int), ("mem_budget", C.c_double)]
+                ("alpha", C.c_double), ("o_max", C.c_int), ("mem_budget", C.c_double),
+                ("prefill_separate", C.c_int)]
 
 
 class SDError(RuntimeError):

@@ -20,6 +20,7 @@ struct Ctx {
   Model d, v;
   double c1d, c2d, c1v, c2v, alpha, mem;
   int o_max;
+  bool prefill_separate;
 };
 
 bool model_ok(const sd_sched_model& m) { return m.n_layers >= 1 && m.d_model >= 1 && m.d_ffn >= 1; }
@@ -37,6 +38,7 @@ bool make_ctx(const sd_sched_cfg* c, Ctx& x) {
   x.alpha = c->alpha;
   x.mem = c->mem_budget;
   x.o_max = c->o_max;
+  x.prefill_separate = c->prefill_separate != 0;
   return true;
 }
 
@@ -62,8 +64,23 @@ double flops_v(const Model& m, double Im, int l, int n, double L) {
 
 // (T^d, T^v) of a batch of b tasks with input length Im at step n
 // (eqs. latency_b2, d_latency, v_latency)
+// decoding-stage forms: one draft token over kv cached tokens; 1 + l verify
+// tokens over kv cached tokens
+double flops_d_decode(const Model& m, double kv) { return 4.0 * m.J * m.h1 * (2.0 * m.h1 + kv + 1.0 + m.h2); }
+double flops_v_decode(const Model& m, double kv, int l) {
+  return 4.0 * m.J * m.h1 * (1.0 + l) * (2.0 * m.h1 + kv + l + 1.0 + m.h2);
+}
+
 std::pair<double, double> step_times(const Ctx& x, int b, double Im, int l, int n, double L) {
   double td = 0.0;
+  if (x.prefill_separate) {
+    // every step is a decoding step: before step n the caches hold the prompt
+    // minus one token plus (n - 1) L emitted tokens
+    const double base = Im - 1.0 + (n - 1) * L;
+    for (int i = 1; i <= l; ++i) td += x.c1d * flops_d_decode(x.d, base + i - 1) * b + x.c2d;
+    const double tv = x.c1v * flops_v_decode(x.v, base, l) * b + x.c2v;
+    return {td, tv};
+  }
   for (int i = 1; i <= l; ++i) td += x.c1d * flops_d(x.d, Im, i, n, L) * b + x.c2d;
   const double tv = x.c1v * flops_v(x.v, Im, l, n, L) * b + x.c2v;
   return {td, tv};

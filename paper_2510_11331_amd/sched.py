@@ -8,6 +8,7 @@ A scheduler configuration is a dict:
   alpha           acceptance rate
   o_max           output tokens given to every task
   mem_budget      draft memory budget in bytes (optional, <= 0: none)
+  prefill_separate  prompts processed before step 1 (optional, default False)
 """
 from __future__ import annotations
 
@@ -28,6 +29,7 @@ def _cfg(cfg: Dict) -> _lib.SchedCfg:
     c.alpha = float(cfg["alpha"])
     c.o_max = int(cfg["o_max"])
     c.mem_budget = float(cfg.get("mem_budget", 0.0))
+    c.prefill_separate = int(bool(cfg.get("prefill_separate", False)))
     return c
 
 

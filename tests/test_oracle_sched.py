@@ -176,3 +176,27 @@ def test_uplink_allocation_equalises_and_beats_perturbations():
         s = sum(v)
         v = [x / s for x in v]
         assert max(S.upload_times(lengths, snr, v, lam, bw)) >= t_star * (1 - 1e-12)
+
+
+def test_prefill_separate_changes_only_the_first_step():
+    sep = dict(CFG, prefill_separate=True)
+    J, h1, h2 = CFG["draft"]
+    Jv, h1v, h2v = CFG["target"]
+    for I_m, l, L in ((40, 3, 2.2), (300, 1, 1.8)):
+        for n in (2, 3, 7):
+            assert S.step_times(sep, 4, I_m, l, n, L) == pytest.approx(S.step_times(CFG, 4, I_m, l, n, L), rel=1e-14)
+        # step 1: l draft forwards of one token over I_m - 1, I_m, ... cached
+        # tokens, and a verify of 1 + l tokens over I_m - 1 cached tokens,
+        # counted product by product
+        b = 4
+        td = sum(CFG["c_draft"][0] * J * block_flops(h1, h2, 1, I_m - 1 + i) * b + CFG["c_draft"][1]
+                 for i in range(1, l + 1))
+        tv = CFG["c_verify"][0] * Jv * block_flops(h1v, h2v, 1 + l, I_m - 1 + l + 1) * b + CFG["c_verify"][1]
+        got = S.step_times(sep, b, I_m, l, 1, L)
+        assert got[0] == pytest.approx(td, rel=1e-12) and got[1] == pytest.approx(tv, rel=1e-12)
+    rng = random.Random(8)
+    lengths = [rng.choice([rng.randint(1, 40), rng.randint(300, 512)]) for _ in range(6)]
+    split = dict(SPLIT, prefill_separate=True)
+    batches, t = S.dp_batching(split, lengths, 3, 0.8, 64)
+    assert t == pytest.approx(S.pipeline_latency(split, batches, lengths, 3, 0.8, 64), rel=1e-12)
+    assert t >= S.brute_force_batching(split, lengths, 3, 0.8, 64)[1] * (1 - 1e-12)

@@ -25,7 +25,7 @@ def canon(batches):
 def cases():
     rng = random.Random(17)
     for trial in range(10):
-        cfg = dict(rng.choice([PAPER, SPLIT]))
+        cfg = dict(rng.choice([PAPER, SPLIT]), prefill_separate=trial % 3 == 2)
         K = rng.randint(1, 14)
         lengths = [rng.choice([rng.randint(1, 64), rng.randint(1, 2048)]) for _ in range(K)]
         alpha = rng.choice([0.0, 0.5, 0.8, 1.0])
