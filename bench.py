@@ -61,7 +61,7 @@ def parse():
 
 
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "pmc_traffic.json")
-GATEUP_NAME = "gemm_kernel<unsigned short, 3, 2, 2, 2>"   # bf16 bits, MT=3, NT=2, U=2, SwiGLU epilogue
+GATEUP_NAME = "gemm_kernel<unsigned short, 3, 6, 2, 2>"   # bf16 bits, MT=3, NT=6 (balanced), U=2, SwiGLU
 COPY_NAME = "neg_kernel"                            # torch.neg over 1 GiB of int16
 COPY_BYTES = 1 << 30
 
@@ -280,6 +280,27 @@ def replay_ms(graph, n):
         ev[k + 1].record()
     torch.cuda.synchronize()
     return float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(n)]))
+
+
+def gateup_kernel_name(M: int, N: int) -> str:
+    """Kernel the library launches for a bf16 SwiGLU gate/up projection of M
+    rows and N = 2 d_ffn columns (the tile choices of plan_gemm / plan_rows)."""
+    if M > 64 and N >= 8192:
+        best, pad = 6, 1 << 30
+        if M <= 640:
+            for c in (4, 5, 6):
+                rows = -(-M // (32 * c)) * 32 * c
+                if rows <= pad:
+                    best, pad = c, rows
+        return f"gemm_rows_kernel<{best}, {4 if N % 128 == 0 else 2}, 2>"
+    if M > 64:
+        return "gemm_kernel<unsigned short, 4, 2, 2, 2>"
+    mt = -(-M // 16)
+    units = N // 32
+    most = -(-units // 256) * 2
+    if mt == 3 and units >= 256 and most <= 6:
+        return f"gemm_kernel<unsigned short, 3, {4 if most <= 4 else 6}, 2, 2> (balanced, 256 workgroups)"
+    return f"gemm_kernel<unsigned short, {mt}, {4 if mt == 3 and units < 512 else 2}, 2, 2>"
 
 
 def fit_runtime(out_json: str) -> None:
@@ -604,8 +625,7 @@ def main():
     verify_p50 = float(np.median(verify_ms))
 
     M = B * (gamma + 1)
-    mt = 4 if M > 64 else (M + 15) // 16
-    gu_name = f"gemm_kernel<unsigned short, {mt}, 2, 2, 2>"
+    gu_name = gateup_kernel_name(M, 2 * t.d_ffn)
     shape_desc = (f"{t.n_layers}-layer d{t.d_model} target ({t.n_heads}/{t.n_kv_heads} heads, FFN {t.d_ffn}) + "
                   f"{d.n_layers}-layer d{d.d_model} draft")
     res = {

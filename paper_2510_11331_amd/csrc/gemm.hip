@@ -9,9 +9,14 @@
 //     fragment load of a wave is one contiguous 1 KB block;
 //   * a workgroup owns one column tile (16*NT output columns = 16*NT rows
 //     of W; NT in {1, 2, 3, 4}, wider tiles re-read the activations less
-//     often) and splits K over its KW waves (up to 16), interleaved in
+//     often) and splits K over its KW waves (up to 4), interleaved in
 //     groups of U k-steps; each wave streams its share of the tile straight
 //     into registers, one step group ahead of the MFMAs;
+//   * or, in balanced mode (one M block), the grid is one workgroup per CU
+//     and the N / 16 column tiles are dealt out evenly, up to NT = 6 per
+//     workgroup: at 33-48 rows the activation re-reads from L2 then cost a
+//     third as much, and no CU holds more work than another by more than
+//     one deal unit;
 //   * the matching activation fragments are loaded the same way (they are
 //     small and stay in L2), so the main loop has no LDS traffic and no
 //     barriers; it has no branches either (padding rows and groups past a
@@ -19,7 +24,7 @@
 //     vmcnt only ever waits for the older step group;
 //   * bf16: one v_mfma_f32_16x16x32_bf16 per 16-byte unit; fp32: four
 //     v_mfma_f32_16x16x4_f32;
-//   * the KW partial tiles are added in wave order through LDS
+//   * the KW partial tiles are added in wave order through LDS in one round
 //     (deterministic); K is never split across workgroups (a cross-workgroup
 //     reduction needs a device-scope release per workgroup, which costs more
 //     than it recovers at these sizes);
@@ -62,11 +67,12 @@ template <> struct Mfma<float> {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
 
-// narrow tiles fit 128 VGPRs and run up to 16 waves; wider ones up to 8
+// register budget the compiler plans for: narrow tiles as for 16 waves
+// (128 VGPRs, several workgroups per CU), wider ones as for 8 (256 VGPRs);
+// a launch runs at most 4 waves
 template <int MT, int NT> struct GemmBounds {
   static constexpr int threads = (MT * NT <= 4 && MT < 4 && NT < 4) ? 1024 : 512;
 };
-int gemm_max_waves(int mt, int nt) { return (mt * nt <= 4 && mt < 4 && nt < 4) ? 16 : 8; }
 
 // Buffer resource over `bytes` bytes at p: raw (unswizzled) addressing with
 // range checking, so a load at an offset >= bytes returns zero and reads no
@@ -144,7 +150,6 @@ __device__ __forceinline__ void qkv_store(const RopeParams& rp, int m, int pos, 
 // from pulling the loads next to their uses).
 template <typename T, int MT, int NT, int U, int EPI>
 __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(GemmParams p) {
-  __shared__ float red[4][MT * NT * 4][64];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -168,10 +173,22 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     bx = (j / p.mblocks) * 8 + (w & 7);
   }
   const bool stream_w = p.mblocks <= 1;
-  const int n0 = bx * 16 * NT;
+  // Balanced mode (p.tile_unit > 0): the N / 16 column tiles, in units of
+  // tile_unit tiles (2 for SwiGLU: a gate tile and its up tile), are dealt
+  // to the gridDim.x workgroups as evenly as possible, a contiguous run per
+  // workgroup of at most NT tiles.  Loads of tiles past the run fall outside
+  // the buffer range: they return zero and read nothing.
+  int tile0 = bx * NT, ntile = NT;
+  if (p.tile_unit > 0) {
+    const int units = p.N / (16 * p.tile_unit), G = gridDim.x;
+    const int base = units / G, extra = units % G;
+    tile0 = (bx * base + min(bx, extra)) * p.tile_unit;
+    ntile = (base + (bx < extra ? 1 : 0)) * p.tile_unit;
+  }
+  const int n0 = tile0 * 16;
   const int m0 = bz * MT * 16;
   const uint32_t tile_bytes = (uint32_t)ksteps * 1024u;
-  const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)p.W + (size_t)bx * NT * tile_bytes, NT * tile_bytes);
+  const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)p.W + (size_t)tile0 * tile_bytes, ntile * tile_bytes);
   const __amdgpu_buffer_rsrc_t ar = buf_rsrc((const char*)p.A + (size_t)bz * MT * tile_bytes, MT * tile_bytes);
 
   f32x4 acc[MT][NT];
@@ -250,93 +267,132 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
         qcs[i][j] = qpos[i] >= 0 && qkind[j] < 2 ? p.rope.tab[(size_t)qpos[i] * half + qf[j]] : float2{1.f, 0.f};
   }
 
-  // Reduction over the KW wave partials, in a fixed order: waves 4.. fold
-  // into waves 0..3 four at a time (slot w holds wave w + base), then waves
-  // 0..3 publish their sums and every wave finishes the output rows (i, v)
-  // with (4 i + v) % KW == wave, adding the four slots in order.
-  for (int base = 4; base < KW; base += 4) {
-    if (wave >= base && wave < base + 4) {
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NT; ++j)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) red[wave - base][(i * NT + j) * 4 + v][lane] = acc[i][j][v];
-    }
-    __syncthreads();
-    if (wave < 4 && wave + base < KW) {
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NT; ++j)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) acc[i][j][v] += red[wave][(i * NT + j) * 4 + v][lane];
-    }
-    __syncthreads();
-  }
-  const int nslot = min(KW, 4);
-  if (wave < nslot) {
+  // Reduction over the KW (<= 4) wave partials, in wave order 0, 1, 2, 3
+  // (deterministic).  Finishing units are a gate/up tile pair (SwiGLU) or a
+  // tile; with at least 4 of them each wave finishes whole units (one LDS
+  // round, 16 bytes per lane), else each finishes output rows.
+  constexpr int TPU = EPI == EPI_SWIGLU ? 2 : 1;        // tiles per unit
+  constexpr int UPR = NT / TPU;                         // units per row tile
+  if constexpr (EPI == EPI_QKV || MT * UPR < 4) {
+    // every wave publishes its partial tile set; wave w finishes the output
+    // rows (i, v) with (4 i + v) % KW == w (for QKV the rows whose
+    // positions, KV blocks and rotary inputs it prefetched)
+    __shared__ float red[4][MT * NT * 4][64];     // [wave][element][lane]
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int j = 0; j < NT; ++j)
 #pragma unroll
         for (int v = 0; v < 4; ++v) red[wave][(i * NT + j) * 4 + v][lane] = acc[i][j][v];
-  }
-  __syncthreads();
-  if constexpr (EPI == EPI_QKV) {
-    // first use of the prefetched rotary inputs before any store: the wait
-    // for them is taken here, not behind the epilogue's stores (the memory
-    // counter also counts stores)
+    __syncthreads();
+    if constexpr (EPI == EPI_QKV) {
+      // first use of the prefetched rotary inputs before any store: the wait
+      // for them is taken here, not behind the epilogue's stores (the memory
+      // counter also counts stores)
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      asm volatile("" : "+v"(qpos[i]), "+v"(qblk[i]));
+      for (int i = 0; i < MT; ++i) {
+        asm volatile("" : "+v"(qpos[i]), "+v"(qblk[i]));
 #pragma unroll
-      for (int j = 0; j < NT; ++j) asm volatile("" : "+v"(qcs[i][j].x), "+v"(qcs[i][j].y));
+        for (int j = 0; j < NT; ++j) asm volatile("" : "+v"(qcs[i][j].x), "+v"(qcs[i][j].y));
+      }
     }
-  }
-
-  // output element (i, j, v) is row m0 + 16 i + 4 g + v, column n0 + 16 j + r16
+    // output element (i, j, v) is row m0 + 16 i + 4 g + v, column n0 + 16 j + r16
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      if ((4 * i + v) % KW != wave) continue;
-      const int m = m0 + 16 * i + 4 * g + v;
-      float o[NT];
-#pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        float t = red[0][(i * NT + j) * 4 + v][lane];
-        for (int w = 1; w < nslot; ++w) t += red[w][(i * NT + j) * 4 + v][lane];
-        o[j] = t;
-      }
-      // QKV: the rotary partner of column r16 is column r16 ^ 8 of the same
-      // tile (exchanged while the whole wave is still converged)
-      float pr[EPI == EPI_QKV ? NT : 1];
-      if constexpr (EPI == EPI_QKV) {
-#pragma unroll
-        for (int j = 0; j < NT; ++j) pr[j] = __shfl_xor(o[j], 8);
-      }
-      if (m >= p.M) continue;
-      if constexpr (EPI == EPI_QKV) {
-        if (qpos[i] < 0) continue;              // row without an input (no pending draft token)
-        qkv_store<T, NT>(p.rope, m, qpos[i], qblk[i], r16, o, pr, qcs[i], qkind, qcol, qkvb);
-      } else if constexpr (EPI == EPI_SWIGLU) {
-        // tiles (2k, 2k+1) are the gate and up rows of the same 16 outputs
-        const int F = p.N / 2;
-#pragma unroll
-        for (int j = 0; j < NT; j += 2)
-          Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F), silu(o[j]) * o[j + 1]);
-      } else {
-        const size_t row = EPI == EPI_PART ? (size_t)blockIdx.y * p.M + m : (size_t)m;
+      for (int v = 0; v < 4; ++v) {
+        if ((4 * i + v) % KW != wave) continue;
+        const int m = m0 + 16 * i + 4 * g + v;
+        float o[NT];
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
-          float* dst = p.out + row * p.ldo + n0 + 16 * j + r16;
-          if constexpr (EPI == EPI_RESID) *dst += o[j];
-          else *dst = o[j];
+          float t = red[0][(i * NT + j) * 4 + v][lane];
+          for (int w = 1; w < KW; ++w) t += red[w][(i * NT + j) * 4 + v][lane];
+          o[j] = t;
+        }
+        if constexpr (EPI == EPI_QKV) {
+          // the rotary partner of column r16 is column r16 ^ 8 of the same
+          // tile (exchanged while the whole wave is still converged)
+          float pr[NT];
+#pragma unroll
+          for (int j = 0; j < NT; ++j) pr[j] = __shfl_xor(o[j], 8);
+          if (m >= p.M || qpos[i] < 0) continue;   // padding row, or no pending draft token
+          qkv_store<T, NT>(p.rope, m, qpos[i], qblk[i], r16, o, pr, qcs[i], qkind, qcol, qkvb);
+        } else if constexpr (EPI == EPI_SWIGLU) {
+          if (m >= p.M) continue;
+          // tiles (2k, 2k+1) are the gate and up rows of the same 16 outputs
+          const int F = p.N / 2;
+#pragma unroll
+          for (int j = 0; j < NT; j += 2)
+            if (j < ntile) Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F), silu(o[j]) * o[j + 1]);
+        } else {
+          if (m >= p.M) continue;
+          const size_t row = EPI == EPI_PART ? (size_t)blockIdx.y * p.M + m : (size_t)m;
+#pragma unroll
+          for (int j = 0; j < NT; ++j) {
+            if (j >= ntile) continue;
+            float* dst = p.out + row * p.ldo + n0 + 16 * j + r16;
+            if constexpr (EPI == EPI_RESID) *dst += o[j];
+            else *dst = o[j];
+          }
         }
       }
-    }
+  } else {
+    // unit u (row tile i, unit k of it) is finished by wave u % KW; the
+    // other waves leave their partial of its tiles in LDS slot
+    // (w - f - 1) mod 4
+    __shared__ f32x4 red[MT * NT][3][64];           // [tile][slot][lane]
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int f = (i * UPR + j / TPU) % KW;
+        if (wave != f && j < ntile) red[i * NT + j][(wave - f - 1) & 3][lane] = acc[i][j];
+      }
+    __syncthreads();
+    // the sum of a tile in wave order 0, 1, 2, 3; this wave's own partial
+    // from registers, the others from their slots
+    auto total = [&](const f32x4& own, int tile) {
+      f32x4 t = own;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if (w >= KW) break;
+        f32x4 pw;
+        if (w == wave) pw = own;
+        else pw = red[tile][(w - wave - 1) & 3][lane];
+        t = w == 0 ? pw : t + pw;
+      }
+      return t;
+    };
+    // output element (i, j, v) is row m0 + 16 i + 4 g + v, column n0 + 16 j + r16
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int k = 0; k < UPR; ++k) {
+        if ((i * UPR + k) % KW != wave || k * TPU >= ntile) continue;
+        if constexpr (EPI == EPI_SWIGLU) {
+          // tiles (2k, 2k+1) are the gate and up rows of the same 16 outputs
+          const f32x4 gt = total(acc[i][2 * k], i * NT + 2 * k), up = total(acc[i][2 * k + 1], i * NT + 2 * k + 1);
+          const int F = p.N / 2;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int m = m0 + 16 * i + 4 * g + v;
+            if (m < p.M) Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 16 * k + r16, F), silu(gt[v]) * up[v]);
+          }
+        } else {
+          const f32x4 o = total(acc[i][k], i * NT + k);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int m = m0 + 16 * i + 4 * g + v;
+            if (m >= p.M) continue;
+            const size_t row = EPI == EPI_PART ? (size_t)blockIdx.y * p.M + m : (size_t)m;
+            float* dst = p.out + row * p.ldo + n0 + 16 * k + r16;
+            if constexpr (EPI == EPI_RESID) *dst += o[v];
+            else *dst = o[v];
+          }
+        }
+      }
+  }
 }
 
 // Row-tiled GEMM for passes with more than one 64-row block (batched
@@ -561,7 +617,7 @@ static hipError_t launch_mt(int mt, dim3 grid, int threads, const GemmParams& p,
     case 1: launch_k(gemm_kernel<T, 1, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p); break;
     case 2: launch_k(gemm_kernel<T, 2, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p); break;
     case 3:
-      if constexpr (NT <= 4) {
+      if constexpr (NT <= 4 || NT == 6) {
         launch_k(gemm_kernel<T, 3, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p);
         break;
       }
@@ -591,18 +647,48 @@ static hipError_t launch_nt(int nt, int mt, dim3 grid, int threads, const GemmPa
       if constexpr (EPI == EPI_QKV) return launch_mt<T, EPI, 3, GEMM_U>(mt, grid, threads, p, s, e0, e1);
       return hipErrorInvalidValue;
     case 4: return launch_mt<T, EPI, 4, GEMM_U>(mt, grid, threads, p, s, e0, e1);
+    // balanced mode at 33-48 rows: SwiGLU up to 3 gate/up pairs
+    case 6:
+      if constexpr (EPI == EPI_SWIGLU && sizeof(T) == 2) return launch_mt<T, EPI, 6, GEMM_U>(mt, grid, threads, p, s, e0, e1);
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }
 
+bool gemm_config_ok(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
+                    const GemmParams& p) {
+  const size_t kbytes = (size_t)p.K * (dtype == 0 ? 2 : 4);
+  if (mt < 1 || mt > 4 || kw < 1 || kw > 4) return false;
+  // instantiated tiles: 48 columns for QKV only, 96 columns (bf16 SwiGLU,
+  // at most 3 row tiles) for balanced mode only
+  switch (nt) {
+    case 1: if (epi == EPI_SWIGLU) return false; break;
+    case 2: break;
+    case 3: if (epi != EPI_QKV || mt > 3) return false; break;
+    case 4: if (mt > 3) return false; break;
+    case 6: if (epi != EPI_SWIGLU || dtype != 0 || mt > 3 || p.tile_unit <= 0) return false; break;
+    default: return false;
+  }
+  if (mt == 4 && nt > 2) return false;
+  if (p.tile_unit > 0) {
+    // balanced mode: one M block, no K split, every workgroup within nt tiles
+    if (p.tile_unit > 2 || p.N % (16 * p.tile_unit) || grid_x < 1 || grid_z != 1 || ksplit != 1 ||
+        epi == EPI_QKV || epi == EPI_PART || (epi == EPI_SWIGLU && p.tile_unit != 2))
+      return false;
+    const int units = p.N / (16 * p.tile_unit);
+    if (units < grid_x || (units + grid_x - 1) / grid_x * p.tile_unit > nt) return false;
+  } else if (p.N % (16 * nt) || grid_x * 16 * nt != p.N) {
+    return false;
+  }
+  if (grid_z * 16 * mt < p.M || kbytes % GEMM_CHUNK) return false;
+  if (ksplit < 1 || (ksplit > 1 && epi != EPI_PART) || ksplit > (int)(kbytes / GEMM_CHUNK)) return false;
+  if (epi == EPI_QKV && (kw != 4 || p.rope.hd % 16 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd)) return false;
+  return true;
+}
+
 hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
                        const GemmParams& p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  if (kw < 1 || kw > gemm_max_waves(mt, nt)) return hipErrorInvalidValue;
-  if (p.N % (16 * nt) || grid_x * 16 * nt != p.N || grid_z * 16 * mt < p.M ||
-      ((size_t)p.K * (dtype == 0 ? 2 : 4)) % GEMM_CHUNK)
-    return hipErrorInvalidValue;
-  if (ksplit < 1 || (ksplit > 1 && epi != EPI_PART) || ksplit > (int)((size_t)p.K * (dtype == 0 ? 2 : 4) / GEMM_CHUNK))
-    return hipErrorInvalidValue;
+  if (!gemm_config_ok(dtype, epi, nt, mt, kw, grid_x, ksplit, grid_z, p)) return hipErrorInvalidValue;
   // several M blocks over column tiles in groups of 8: the XCD-aware 1-D grid
   GemmParams q = p;
   q.mblocks = 1;
@@ -612,8 +698,6 @@ hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, i
     grid = dim3(grid_x * grid_z, 1, 1);
   }
   const int threads = 64 * kw;
-  if (epi == EPI_QKV && (kw != 4 || p.rope.hd % 16 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd))
-    return hipErrorInvalidValue;
   if (dtype == 0) {
     if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, q, s, e0, e1);
     if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, q, s, e0, e1);

@@ -280,6 +280,7 @@ void prof_end(sd_ctx* ctx, hipStream_t s, ProfRec& r) {
 
 struct GemmPlan {
   int nt, mt, kw, gx, ksplit, gz;
+  int tu;   // > 0: balanced column tiles dealt in units of tu tiles over gx = 256 workgroups
 };
 
 // One column tile of 16*nt columns per workgroup, kw waves splitting K inside
@@ -290,7 +291,14 @@ struct GemmPlan {
 //     than noise, often worse);
 //   * QKV: 48-column tiles when that gives 192 ... 320 workgroups (7B width:
 //     one per CU, 20 us against 25 us for 32-column tiles), else 16-column;
-//   * SwiGLU gate/up: 64-column tiles for 3-tile row blocks with < 512
+//   * 3-tile row blocks (33-48 rows, bf16): gate/up (SwiGLU) in balanced
+//     mode, one workgroup per CU with the gate/up tile pairs dealt out
+//     evenly (up to 3 pairs; 7B gate/up 38.4 -> 35.5 us): at these rows the
+//     activation re-reads from L2 that a 32-column tile costs per weight
+//     byte are what limit the shape.  The LM head gained nothing from it
+//     (8 tiles per workgroup), nor the down projection from 64-column tiles
+//     split 4 ways over K (the RMSNorm adding 4 partial sums cost more);
+//   * other SwiGLU gate/up: 64-column tiles for 3-tile row blocks with < 512
 //     column pairs (fewer activation re-reads), else 32-column;
 //   * residual projections (O, down) with an RMSNorm after them (split_ok)
 //     and one row block: K split over workgroups until there are ~256 of
@@ -309,10 +317,21 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
   g.mt = g.gz > 1 ? 4 : (M + 15) / 16;
   g.ksplit = 1;
   g.kw = 4;
+  g.tu = 0;
   const int groups = (int)(K * esz / 64) / GEMM_U;   // k-step groups of one wave step
   auto pick = [&](int nt) { return N % (16 * nt) == 0; };
+  // balanced mode: tiles of tu over 256 workgroups, at most nt_max per workgroup
+  auto balanced = [&](int tu, int nt_max) {
+    if (g.gz != 1 || g.mt != 3 || esz != 2 || N % (16 * tu)) return 0;
+    const int units = N / (16 * tu), most = (units + 255) / 256 * tu;
+    if (units < 256 || most > nt_max) return 0;
+    return most <= 4 ? 4 : nt_max;
+  };
   if (g.gz > 1) {
     g.nt = pick(2) ? 2 : 1;
+  } else if (epi == EPI_SWIGLU && balanced(2, 6)) {
+    g.nt = balanced(2, 6);
+    g.tu = 2;
   } else if (epi == EPI_SWIGLU) {
     g.nt = (g.mt == 3 && pick(4) && N / 32 < 512) ? 4 : 2;
   } else if (epi == EPI_QKV) {
@@ -330,7 +349,7 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
   } else {
     g.nt = pick(2) ? 2 : 1;
   }
-  g.gx = N / (16 * g.nt);
+  g.gx = g.tu ? 256 : N / (16 * g.nt);
   const int gps = (groups + g.ksplit - 1) / g.ksplit;
   // the QKV epilogue assigns output rows by wave and needs exactly 4 waves
   if (epi != EPI_QKV) g.kw = std::max(1, std::min(g.kw, gps / 2));
@@ -372,7 +391,7 @@ int gemm(sd_ctx* ctx, const ModelRT& m, int epi, const void* A, const void* W, i
          float* out, int ldo, void* out_t, hipStream_t s, int prof_kind, int prof_kind2,
          const RopeParams* rope = nullptr, float* part = nullptr, int* nsplit = nullptr) {
   GemmPlan g = plan_gemm(M, N, K, m.esz, epi, part != nullptr);
-  if (N % (16 * g.nt)) return SD_EINVAL;
+  if (!g.tu && N % (16 * g.nt)) return SD_EINVAL;
   if (nsplit) *nsplit = 0;
   if (g.ksplit > 1) {
     epi = EPI_PART;
@@ -388,6 +407,7 @@ int gemm(sd_ctx* ctx, const ModelRT& m, int epi, const void* A, const void* W, i
   p.out = out;
   p.ldo = ldo;
   p.out_t = out_t;
+  p.tile_unit = g.tu;
   if (rope) p.rope = *rope;
   const double out_bytes = epi == EPI_SWIGLU ? (double)M * (N / 2) * m.esz
                            : epi == EPI_QKV  ? (double)M * (m.nq() * 4 + (N - m.nq()) * m.esz)

@@ -147,6 +147,7 @@ struct GemmParams {
   void* out_t;        // SWIGLU: out_t[M, N/2] in the MFMA-tile layout
   RopeParams rope;    // QKV: rotary embedding of q and k, K/V appended to the cache
   int mblocks;        // > 1: 1-D grid of (column tile, M block) pairs, XCD-aware (see gemm.hip)
+  int tile_unit;      // > 0: balanced column tiles, dealt in units of tile_unit tiles (see gemm.hip)
 };
 
 struct AttnParams {
@@ -222,12 +223,14 @@ inline void launch_k(K kern, dim3 grid, dim3 block, uint32_t shm, hipStream_t s,
   else hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
 }
 
-int gemm_max_waves(int mt, int nt);   // waves per workgroup the (mt, nt) tile allows
 // Row-tiled bf16 GEMM for passes of several 64-row blocks: 32 mf x 32 nf
 // output tiles, mf in {4, 5, 6, 8}, nf in {2, 4}; epi: STORE, RESID, SWIGLU
 // or QKV (no K split).  N must be a multiple of 32 nf.
 hipError_t launch_gemm_rows(int epi, int mf, int nf, const GemmParams& p, hipStream_t s, hipEvent_t e0 = nullptr,
                             hipEvent_t e1 = nullptr);
+// Host-side check of a skinny GEMM launch (launch_gemm rejects what fails it)
+bool gemm_config_ok(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
+                    const GemmParams& p);
 hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, int ksplit, int grid_z,
                        const GemmParams& p, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // tab[pos * half + i] = (cos, sin) of pos * theta^(-i/half), pos < n_pos, i < half
