@@ -231,8 +231,8 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
   };
 
   // QKV runs exactly 4 waves, so wave w finishes the rows 16 i + 4 g + w of
-  // the block; their positions and KV blocks are loaded before the stream
-  // and their rotary (cos, sin) after it, so the epilogue waits on nothing
+  // the block; their positions, KV blocks and rotary (cos, sin) are loaded
+  // at the start of the stream, so the epilogue waits on nothing
   int qpos[EPI == EPI_QKV ? MT : 1], qblk[EPI == EPI_QKV ? MT : 1];
   if constexpr (EPI == EPI_QKV) {
 #pragma unroll
@@ -243,20 +243,19 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     }
   }
 
-  // groups past nw load zeros (no memory access) and add nothing
-  load.template operator()<0>(0);
-  for (int i = 0; i < nw; i += 2) {
-    load.template operator()<1>(i + 1);
-    compute.template operator()<0>();
-    load.template operator()<0>(i + 2);
-    compute.template operator()<1>();
-  }
-
   // QKV: what column n0 + 16 j + r16 of this lane is (independent of the row)
   int qkind[EPI == EPI_QKV ? NT : 1], qcol[EPI == EPI_QKV ? NT : 1], qf[EPI == EPI_QKV ? NT : 1];
   size_t qkvb[EPI == EPI_QKV ? NT : 1];
   float2 qcs[EPI == EPI_QKV ? MT : 1][NT];
+
+  // groups past nw load zeros (no memory access) and add nothing
+  load.template operator()<0>(0);
   if constexpr (EPI == EPI_QKV) {
+    // the rotary (cos, sin) of this lane's rows are loaded once both register
+    // stages are in flight: the wait for the row positions (loaded first)
+    // then overlaps the first step group's, and the table loads complete
+    // during the stream instead of after it
+    load.template operator()<1>(1);
     const int half = p.rope.hd / 2;
 #pragma unroll
     for (int j = 0; j < NT; ++j) qkv_column<T>(p.rope, n0 + 16 * j, r16, qkind[j], qcol[j], qf[j], qkvb[j]);
@@ -265,6 +264,20 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
 #pragma unroll
       for (int j = 0; j < NT; ++j)
         qcs[i][j] = qpos[i] >= 0 && qkind[j] < 2 ? p.rope.tab[(size_t)qpos[i] * half + qf[j]] : float2{1.f, 0.f};
+    __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < nw; i += 2) {
+      compute.template operator()<0>();
+      load.template operator()<0>(i + 2);
+      compute.template operator()<1>();
+      load.template operator()<1>(i + 3);
+    }
+  } else {
+    for (int i = 0; i < nw; i += 2) {
+      load.template operator()<1>(i + 1);
+      compute.template operator()<0>();
+      load.template operator()<0>(i + 2);
+      compute.template operator()<1>();
+    }
   }
 
   // Reduction over the KW (<= 4) wave partials, in wave order 0, 1, 2, 3
