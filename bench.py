@@ -518,7 +518,7 @@ def main():
               "the single-GPU figure is the per-GPU share of the task-sharded design.", file=sys.stderr)
         sys.exit(2)
     import torch
-    from paper_2510_11331_amd import SDEngine, StepGraph, generate, generate_graph
+    from paper_2510_11331_amd import SDEngine, StepGraph, generate, generate_graph, emitted_tokens
     from paper_2510_11331_amd import _lib
 
     wl = synth.WORKLOADS[args.workload]
@@ -537,7 +537,10 @@ def main():
         lens = [wl.prompt_len] * n_tasks
         prompt_desc = f"prompt {wl.prompt_len}"
     max_new = (2 * K + W + 2) * (gamma + 1)
-    ctx_need = max(lens) + max_new + gamma + 16
+    forced = wl.alpha_forced is not None
+    # a forced-acceptance workload first generates its reference continuation
+    # (the target's greedy output) with up to max_new unforced steps
+    ctx_need = max(lens) + (2 if forced else 1) * max_new + gamma + 16
     print(f"[bench] workload {wl.name} B={B}x{n_batches} gamma={gamma} steps={K} warmup={W}", file=sys.stderr,
           flush=True)
 
@@ -550,11 +553,28 @@ def main():
 
     prompts = synth.prompts(n_tasks, lens, t.vocab)
     t0 = time.time()
-    eng.prefill(list(range(n_tasks)), prompts, [max_new] * n_tasks)
+    eng.prefill(list(range(n_tasks)), prompts, [(2 if forced else 1) * max_new] * n_tasks)
     print(f"[bench] prefill {n_tasks} tasks, {sum(lens)} tokens in {time.time() - t0:.2f}s", file=sys.stderr,
           flush=True)
 
     batches = [eng.batch(list(range(m * B, (m + 1) * B)), gamma) for m in range(n_batches)]
+    if forced:
+        # greedy verification emits the target's greedy continuation whatever
+        # the drafts, so one unforced run gives each task's continuation; the
+        # timed run then starts over with drafts forced to it w.p. alpha
+        assert n_batches == 1 and wl.greedy
+        t0 = time.time()
+        ref = eng.batch(list(range(B)), gamma)
+        acc0, out0 = generate_graph(eng, ref, synth.uniform_table(7, list(range(B)), max_new, gamma), max_new)
+        em = emitted_tokens(acc0, out0)
+        assert min(len(e) for e in em) >= max_new
+        cont = np.array([list(prompts[k]) + em[k][:max_new] for k in range(B)], dtype=np.int32)
+        for s_ in range(n_tasks):
+            eng.release(s_)
+        eng.prefill(list(range(n_tasks)), prompts, [(2 if forced else 1) * max_new] * n_tasks)
+        batches[0].set_force(cont, wl.alpha_forced)
+        print(f"[bench] reference continuation of {max_new} tokens per task in {time.time() - t0:.1f}s; "
+              f"drafts forced with probability {wl.alpha_forced}", file=sys.stderr, flush=True)
     uts = [synth.uniform_table(42, list(range(m * B, (m + 1) * B)), W + 2 * K, gamma) for m in range(n_batches)]
     batch, ut = batches[0], uts[0]
     if args.pmc_pass:
@@ -643,9 +663,11 @@ def main():
         "data": "synthetic: random-init N(0,0.02^2) bf16 weights, uniform-random prompt ids, SplitMix64 uniforms",
         "config": {"workload": f"{shape_desc}, B={B}" + (f" x {n_batches} batches on two streams" if n_batches > 1
                                                             else "") + f", gamma={gamma}, {prompt_desc}, "
-                               f"tau={wl.temperature}",
+                               + (f"greedy verification, drafts forced to the target's greedy continuation "
+                                  f"w.p. {wl.alpha_forced}" if forced else
+                                  "greedy" if wl.greedy else f"tau={wl.temperature}"),
                    "batch": B, "batches": n_batches, "gamma": gamma, "prompt_len": float(np.mean(lens)),
-                   "temperature": wl.temperature},
+                   "temperature": 0.0 if wl.greedy else wl.temperature},
         "verify_ms_p50": round(verify_p50, 3),
         "verify_ms_p90": round(float(np.percentile(verify_ms, 90)), 3),
         "verify_hbm_gbs": round(step_bytes / (verify_p50 * 1e-3) / 1e9, 1),
@@ -655,6 +677,9 @@ def main():
         "draft_ms_per_call": round(float(np.median(draft_ms)) / gamma, 4),
         "mean_accepted": round(float(acc.mean()), 4),
         "mean_emitted_per_step": round(float((acc + 1).mean()), 4),
+        # eq. ol at the forced acceptance rate (chance matches of the draft aside)
+        "emitted_per_step_eq_ol": (round((1 - wl.alpha_forced ** (gamma + 1)) / (1 - wl.alpha_forced), 4)
+                                   if forced and wl.alpha_forced < 1 else None),
         "device_flags": flags,
         "roofline": {"kernel": f"{gu_name} (target FFN gate/up, M={M}, N={2 * t.d_ffn}, K={t.d_model})",
                      "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -196,6 +196,24 @@ int sd_accept_resample(int B, int gamma, int vocab, int greedy,
 int sd_kv_commit(sd_ctx *ctx, int B, const int32_t *slots, int gamma,
                  const int32_t *n_acc, const int32_t *out_tok, void *stream);
 
+/* Forced acceptance, a workload generator for greedy verification (the
+ * acceptance rate alpha of eq. ol set from outside, as random-weight models
+ * give none of their own).  Call between sd_draft_step(i) and the next
+ * draft or verify call of the batch.  For each task b, if its draft uniform
+ * u[b, i] (the slot sd_draft_step(i) read; unused by greedy drafting) is
+ * below alpha 2^32, draft_tok[b, i] is replaced by cont[b, P + i + 1]: the
+ * token that the task's reference continuation (e.g. the target's greedy
+ * output, prompt included, indexed by absolute position, cont_len per task)
+ * holds at that draft's position, P being the committed length.  Positions
+ * at or past cont_len are left alone.  The draft model then consumes the
+ * forced token, and greedy verification accepts it iff it is the target's
+ * arg-max.  cont [B, cont_len] int32, u [B, 2 gamma + 1] uint32 and
+ * draft_tok [B, gamma] are device arrays; 0 <= alpha <= 1.  SD_ESTATE if
+ * the context samples (greedy == 0). */
+int sd_force_draft(sd_ctx *ctx, int B, const int32_t *slots, int gamma, int i,
+                   const int32_t *cont, int cont_len, const uint32_t *u, double alpha,
+                   int32_t *draft_tok, void *stream);
+
 /* Copy slot state to out [B, 4] int32 (device): committed target length
  * P, next input token x0, pending draft input (-1 if none), KV capacity. */
 int sd_slot_state(sd_ctx *ctx, int B, const int32_t *slots, int32_t *out,

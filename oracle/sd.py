@@ -19,8 +19,16 @@ Readings where the paper is silent:
   * Uniform slots per (task, step): 0..gamma-1 draft samples, gamma..2gamma-1
     acceptance tests, 2gamma the residual / reward sample.
   * Emitted tokens beyond a task's budget are discarded (whole steps are run).
+  * Forced acceptance (a workload rule, not part of the method: it sets the
+    acceptance rate alpha of eq. ol from outside on random-weight models):
+    under greedy verification, draft t_{i+1} is replaced, after the draft
+    produced it and before the draft consumes it, by the token a reference
+    continuation holds at its position P + 1 + i when the slot's draft
+    uniform u_i (unused by greedy drafting) is below alpha 2^32.
 """
 from __future__ import annotations
+
+import math
 
 from typing import Dict, List, Optional, Sequence
 
@@ -28,6 +36,13 @@ import numpy as np
 
 from .model import Model, KVCache
 from .sampling import accept_resample, draft_sample, softmax_f32, argmax_lowest, sample_weights
+
+
+def force_threshold(alpha: float) -> int:
+    """alpha as a bound on a uint32 uniform (forced iff u < bound):
+    alpha 2^32 rounded to the nearest integer, halves away from zero."""
+    assert 0.0 <= alpha <= 1.0
+    return int(math.floor(alpha * 4294967296.0 + 0.5))
 
 
 class SDTask:
@@ -51,9 +66,11 @@ class SDTask:
         return len(self.tc)
 
     def step(self, gamma: int, u: np.ndarray, tau: float = 1.0, greedy: bool = False,
-             batch_rows: bool = False, record: Optional[dict] = None):
+             batch_rows: bool = False, record: Optional[dict] = None, force: Optional[tuple] = None):
         """One draft -> verify -> accept -> rollback step with the uniform
-        vector u [2*gamma+1] (uint32).  Returns (a, emitted tokens)."""
+        vector u [2*gamma+1] (uint32).  force = (continuation by absolute
+        position, force_threshold(alpha)) applies forced acceptance (greedy
+        only).  Returns (a, emitted tokens)."""
         P = self.P
         # drafting: pending inputs then x0, then t_1..t_{gamma-1}
         feed = self.pending + [self.x0]
@@ -61,8 +78,14 @@ class SDTask:
         for i, t in enumerate(feed):
             z = self.draft.decode_row(self.dc, t, len(self.dc))
         drafts, qs = [], []
+        assert force is None or greedy
         for i in range(gamma):
             t, q = draft_sample(z, tau, int(u[i]), greedy)
+            if force is not None:
+                cont, bound = force
+                pos = P + 1 + i
+                if int(u[i]) < bound and pos < len(cont):
+                    t = int(cont[pos])
             drafts.append(t)
             qs.append(q)
             if i < gamma - 1:
@@ -90,13 +113,15 @@ class SDTask:
 
 def sd_generate(target: Model, draft: Model, prompt: Sequence[int], gamma: int,
                 n_new: int, utable: np.ndarray, tau: float = 1.0, greedy: bool = False,
-                batch_rows: bool = False, records: Optional[list] = None) -> Dict:
+                batch_rows: bool = False, records: Optional[list] = None,
+                force: Optional[tuple] = None) -> Dict:
     """Speculative decoding of one task until at least n_new tokens are
-    emitted.  utable [n_steps, 2*gamma+1] holds this task's uniforms."""
+    emitted.  utable [n_steps, 2*gamma+1] holds this task's uniforms; force
+    as in SDTask.step."""
     task = SDTask(target, draft, prompt, batch_rows)
     while len(task.emitted) < n_new:
         rec = {} if records is not None else None
-        task.step(gamma, utable[task.n_steps], tau, greedy, batch_rows, rec)
+        task.step(gamma, utable[task.n_steps], tau, greedy, batch_rows, rec, force)
         if records is not None:
             records.append(rec)
     return {"tokens": task.emitted[:n_new], "accepted": task.accepted,

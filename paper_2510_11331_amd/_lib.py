@@ -18,7 +18,7 @@ SD_DTYPE_BF16, SD_DTYPE_F32 = 0, 1
 
 # the symbols include/sd.h and include/sd_sched.h declare (checked by the CPU test suite)
 EXPORTS = ("sd_kv_pool_bytes", "sd_workspace_bytes", "sd_init", "sd_prefill", "sd_release",
-           "sd_draft_step", "sd_verify", "sd_accept_resample", "sd_kv_commit", "sd_slot_state",
+           "sd_draft_step", "sd_verify", "sd_accept_resample", "sd_kv_commit", "sd_force_draft", "sd_slot_state",
            "sd_check", "sd_profile", "sd_profile_read", "sd_destroy", "sd_strerror", "sd_last_error",
            "sd_pack_linear", "sd_sched_latency", "sd_sched_batching", "sd_sched_plan", "sd_sched_uplink")
 
@@ -94,6 +94,7 @@ def lib():
         "sd_verify": (I, [P, I, P, I, P, P, P, P]),
         "sd_accept_resample": (I, [I, I, I, I, P, P, P, P, P, P, P]),
         "sd_kv_commit": (I, [P, I, P, I, P, P, P]),
+        "sd_force_draft": (I, [P, I, P, I, I, P, I, P, C.c_double, P, P]),
         "sd_slot_state": (I, [P, I, P, P, P]),
         "sd_check": (I, [P, P, C.POINTER(C.c_int32)]),
         "sd_profile": (I, [P, I]),

@@ -386,6 +386,28 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
   hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(RT), 0, s, p);
   return hipGetLastError();
 }
+// Forced acceptance for workload generation: with probability alpha (the
+// slot's draft uniform below alpha 2^32) draft token i of a task becomes the
+// token its reference continuation holds at that position (P + i + 1, P the
+// committed length).  Used with greedy verification, where the draft
+// uniforms are otherwise unused.
+__global__ void force_draft_kernel(ForceParams p) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= p.B) return;
+  const int slot = p.slots[b];
+  if (slot < 0 || slot >= p.n_slots) return;
+  const int pos = p.state[(size_t)slot * ST_N + ST_LEN] + p.i + 1;
+  const uint32_t u = p.u[(size_t)b * (2 * p.gamma + 1) + p.i];
+  if ((uint64_t)u < p.threshold && pos >= 0 && pos < p.cont_len)
+    p.draft_tok[(size_t)b * p.gamma + p.i] = p.cont[(size_t)b * p.cont_len + pos];
+}
+
+hipError_t launch_force_draft(const ForceParams& p, hipStream_t s) {
+  if (p.B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(force_draft_kernel, dim3((p.B + 255) / 256), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_commit(const CommitParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
   hipLaunchKernelGGL(commit_kernel, dim3((p.B + 255) / 256), dim3(256), 0, s, p);

@@ -853,6 +853,28 @@ int sd_kv_commit(sd_ctx* ctx, int B, const int32_t* slots, int gamma, const int3
   return SD_OK;
 }
 
+int sd_force_draft(sd_ctx* ctx, int B, const int32_t* slots, int gamma, int i, const int32_t* cont, int cont_len,
+                   const uint32_t* u, double alpha, int32_t* draft_tok, void* stream) {
+  if (!batch_ok(ctx, B, slots, gamma) || i < 0 || i >= gamma || !cont || cont_len < 1 || !u || !draft_tok ||
+      !(alpha >= 0.0 && alpha <= 1.0))
+    return SD_EINVAL;
+  if (!ctx->cfg.greedy) return SD_ESTATE;   // the draft uniforms are in use when sampling
+  ForceParams fp{};
+  fp.B = B;
+  fp.gamma = gamma;
+  fp.i = i;
+  fp.n_slots = ctx->cfg.max_slots;
+  fp.slots = slots;
+  fp.state = ctx->state;
+  fp.cont = cont;
+  fp.cont_len = cont_len;
+  fp.u = u;
+  fp.threshold = (uint64_t)std::llround(alpha * 4294967296.0);
+  fp.draft_tok = draft_tok;
+  HIPCHK(launch_force_draft(fp, (hipStream_t)stream));
+  return SD_OK;
+}
+
 int sd_slot_state(sd_ctx* ctx, int B, const int32_t* slots, int32_t* out, void* stream) {
   if (!ctx || B < 1 || !slots || !out) return SD_EINVAL;
   // gather via the commit-free path: one tiny copy per row on the stream

@@ -205,6 +205,17 @@ struct CommitParams {
   int32_t* err;
 };
 
+struct ForceParams {
+  int B, gamma, i, n_slots;
+  const int32_t* slots;
+  const int32_t* state;
+  const int32_t* cont;     // [B, cont_len] token at each absolute position
+  int cont_len;
+  const uint32_t* u;       // [B, 2 gamma + 1]; slot i decides
+  uint64_t threshold;      // forced iff u < threshold (alpha * 2^32)
+  int32_t* draft_tok;      // [B, gamma]
+};
+
 // PART: K split over gridDim.y workgroups; split y stores its partial sum to
 // out[(y * M + m) * ldo + n], the residual add happens in the next RMSNorm
 enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_PART = 4 };
@@ -241,6 +252,7 @@ hipError_t launch_softmax(const SoftmaxParams& p, hipStream_t s);
 hipError_t launch_draft_sample(const DraftSampleParams& p, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
 hipError_t launch_commit(const CommitParams& p, hipStream_t s);
+hipError_t launch_force_draft(const ForceParams& p, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t s);
 hipError_t launch_pack_linear(int dtype, const void* src, void* dst, int N, int K, hipStream_t s);
 

@@ -123,6 +123,19 @@ class Batch:
         self.p = torch.zeros(B, gamma + 1, vocab, dtype=torch.float32, device=device)
         self.n_acc = torch.zeros(B, dtype=torch.int32, device=device)
         self.out_tok = torch.zeros(B, gamma + 1, dtype=torch.int32, device=device)
+        # forced acceptance (greedy engines only): (cont [B, L] int32 device, alpha)
+        self.force: Optional[tuple] = None
+
+    def set_force(self, cont: Optional[np.ndarray], alpha: float = 0.0, device="cuda") -> None:
+        """Draft token i of task b becomes cont[b, position] with probability
+        alpha (sd_force_draft); cont [B, L] holds each task's reference
+        continuation by absolute position.  None switches forcing off."""
+        if cont is None:
+            self.force = None
+            return
+        c = torch.from_numpy(np.ascontiguousarray(cont, dtype=np.int32)).to(device)
+        assert c.shape[0] == self.B
+        self.force = (c, float(alpha))
 
 
 class SDEngine:
@@ -197,8 +210,14 @@ class SDEngine:
         return Batch(slots, gamma, self.vocab, self.device)
 
     def draft_step(self, b: Batch, i: int, u: torch.Tensor, stream=None) -> None:
+        """Draft call i of the step; with b.force set, followed by the forced
+        acceptance of draft token i (sd_force_draft)."""
         check(self.L.sd_draft_step(self.ctx, b.B, _ptr(b.slots), b.gamma, i, _ptr(u), _ptr(b.draft_tok),
                                    _ptr(b.q), _stream(stream)), "sd_draft_step")
+        if b.force is not None:
+            cont, alpha = b.force
+            check(self.L.sd_force_draft(self.ctx, b.B, _ptr(b.slots), b.gamma, i, _ptr(cont), int(cont.shape[1]),
+                                        _ptr(u), alpha, _ptr(b.draft_tok), _stream(stream)), "sd_force_draft")
 
     def verify(self, b: Batch, logits: Optional[torch.Tensor] = None, stream=None) -> None:
         check(self.L.sd_verify(self.ctx, b.B, _ptr(b.slots), b.gamma, _ptr(b.draft_tok), _ptr(b.p),

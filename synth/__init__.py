@@ -85,6 +85,9 @@ class Workload:
     greedy: bool = False
     prompt_range: Optional[tuple] = None
     kv_block: int = 16
+    # forced acceptance rate (greedy verification, drafts replaced by the
+    # target's greedy continuation with this probability); None: off
+    alpha_forced: Optional[float] = None
 
 
 MODELS: Dict[str, ModelShape] = {
@@ -115,7 +118,7 @@ WORKLOADS: Dict[str, Workload] = {
                          batch=32, prompt_len=0, gamma=4, new_tokens=128,
                          prompt_range=(128, 2048)),
     "13b": Workload("13b", MODELS["13b_target"], MODELS["13b_draft"],
-                    batch=64, prompt_len=512, gamma=4, new_tokens=128),
+                    batch=64, prompt_len=512, gamma=4, new_tokens=128, greedy=True, alpha_forced=0.8),
 }
 
 # --------------------------------------------------------------------------
