@@ -51,6 +51,9 @@ def parse():
                     help="fit the runtime model T(b, F) = c1 F b + c2 of the verify and draft forwards of the "
                          "7B-shape pair on this GPU (graph-replayed passes over batch sizes, contexts and "
                          "speculation lengths), write the fit to OUT_JSON and exit")
+    ap.add_argument("--sweep-gamma", metavar="GAMMAS", default=None,
+                    help="comma-separated speculation lengths: step time, verify / draft latency and tokens per "
+                         "step of --workload at each (one JSON line per length), then exit")
     ap.add_argument("--schedule", metavar="FIT_JSON",
                     help="with a runtime fit: plan batches and speculation length for synthetic task sets, "
                          "compare with the baseline policies (predicted), and run plans on the GPU (measured)")
@@ -472,6 +475,69 @@ def schedule_eval(fit_json: str) -> None:
     print(json.dumps(out), flush=True)
 
 
+def gamma_sweep(args) -> None:
+    """The speculation-length sweep of a workload (7B B = 1: verify latency
+    against gamma; 13B: gamma 2 / 4 / 8): for each gamma a fresh prefill of
+    the same tasks, W warmup and K timed graph replays of the whole step,
+    then the verify pass and the gamma draft calls alone (graph replay, p50)."""
+    import torch
+    from paper_2510_11331_amd import SDEngine, StepGraph, generate_graph, emitted_tokens
+    wl = synth.WORKLOADS[args.workload]
+    gammas = [int(x) for x in args.sweep_gamma.split(",")]
+    B, K, W = args.batch or wl.batch, args.steps, args.warmup
+    t, d = wl.target, wl.draft
+    assert not wl.prompt_range, "one batch of fixed-length prompts"
+    g_max = max(gammas)
+    forced = wl.alpha_forced is not None
+    max_new = (K + W + 2) * (g_max + 1)
+    tg, dg = synth.StreamingWeights(t, 1), synth.StreamingWeights(d, 2)
+    eng = SDEngine(t, d, tg, dg, max_slots=B, max_batch=B, gamma_max=g_max,
+                   max_ctx=wl.prompt_len + 2 * max_new + g_max + 16, prefill_rows=2048,
+                   temperature=wl.temperature, greedy=wl.greedy)
+    tg.close(); dg.close()
+    slots = list(range(B))
+    prompts = synth.prompts(B, wl.prompt_len, t.vocab)
+    cont = None
+    if forced:
+        eng.prefill(slots, prompts, [2 * max_new] * B)
+        ref = eng.batch(slots, 1)
+        acc0, out0 = generate_graph(eng, ref, synth.uniform_table(7, slots, max_new, 1), max_new)
+        em = emitted_tokens(acc0, out0)
+        cont = np.array([list(prompts[k]) + em[k][:max_new] for k in range(B)], dtype=np.int32)
+        for s_ in slots:
+            eng.release(s_)
+    for gamma in gammas:
+        eng.prefill(slots, prompts, [2 * max_new] * B)
+        batch = eng.batch(slots, gamma)
+        if forced:
+            batch.set_force(cont, wl.alpha_forced)
+        ut = synth.uniform_table(42, slots, W + K, gamma)
+        graph = StepGraph(eng, batch)
+        generate_graph(eng, batch, ut[:W], W, graph)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        acc, _ = generate_graph(eng, batch, ut[W:W + K], K, graph)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        del graph
+        verify_ms, draft_ms = graph_latencies(eng, batch, ut[W + K - 1], K)
+        flags = eng.check_flags()
+        emitted = float((acc + 1).mean())
+        line = {"workload": wl.name, "batch": B, "gamma": gamma, "steps": K, "ms_per_step": round(elapsed / K * 1e3, 3),
+                "tokens_per_s": round(float((acc + 1).sum()) / elapsed, 1),
+                "verify_ms_p50": round(float(np.median(verify_ms)), 4),
+                "draft_ms_per_call": round(float(np.median(draft_ms)) / gamma, 4),
+                "mean_emitted_per_step": round(emitted, 4), "device_flags": flags}
+        if forced and wl.alpha_forced < 1:
+            a = wl.alpha_forced
+            line["alpha_forced"] = a
+            line["emitted_per_step_eq_ol"] = round((1 - a ** (gamma + 1)) / (1 - a), 4)
+        print(json.dumps(line), flush=True)
+        for s_ in slots:
+            eng.release(s_)
+    eng.close()
+
+
 def graph_latencies(eng, batch, u_step, n):
     """Median-ready lists of n replay times (ms) of the verify pass and of the
     gamma draft calls of one batch, each captured as a HIP graph."""
@@ -512,6 +578,9 @@ def main():
         return
     if args.schedule:
         schedule_eval(args.schedule)
+        return
+    if args.sweep_gamma:
+        gamma_sweep(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
