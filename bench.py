@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--schedule", metavar="FIT_JSON",
                     help="with a runtime fit: plan batches and speculation length for synthetic task sets, "
                          "compare with the baseline policies (predicted), and run plans on the GPU (measured)")
+    ap.add_argument("--counters-summary", metavar="COUNTER_CSV",
+                    help="markdown per-kernel summary of a rocprofv3 --pmc counter_collection.csv, then exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc counter_collection.csv files of --pmc-pass runs "
                          "(FETCH_SIZE, then WRITE_SIZE) into profiles/pmc_traffic.json and exit")
@@ -189,6 +191,55 @@ def cpu_baseline(wl, B, gamma, emitted_per_step):
             "step_seconds": round(t_step, 4)}
 
 
+def short_kernel_name(n: str) -> str:
+    """"void sd::gemm_kernel<...>(sd::GemmParams) [clone .kd]" -> "sd::gemm_kernel<...>"."""
+    n = n.split(" [clone")[0].strip()
+    if n.startswith("void "):
+        n = n[5:]
+    if n.endswith(")"):
+        depth = 0
+        for i in range(len(n) - 1, -1, -1):
+            depth += n[i] == ")"
+            depth -= n[i] == "("
+            if depth == 0:
+                n = n[:i]
+                break
+    return n
+
+
+def counters_summary(path: str) -> None:
+    """Markdown table of a rocprofv3 --pmc counter_collection.csv: per kernel
+    and grid size, the dispatches, the median duration under counter
+    collection, the median of every collected counter, and for MfmaFlopsBF16
+    the achieved dense bf16 rate against MI355X's 2.5 PFLOP/s."""
+    import csv
+    from collections import defaultdict
+    vals, durs, counters = defaultdict(lambda: defaultdict(list)), defaultdict(dict), []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            key = (short_kernel_name(r["Kernel_Name"]), int(r.get("Grid_Size", 0) or 0))
+            c = r["Counter_Name"]
+            if c not in counters:
+                counters.append(c)
+            vals[key][c].append(float(r["Counter_Value"]))
+            durs[key][r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    head = "| kernel (grid) | dispatches | median us | " + " | ".join(f"median {c}" for c in counters)
+    if "MfmaFlopsBF16" in counters:
+        head += " | bf16 TFLOP/s | of 2.5 PFLOP/s"
+    print(head + " |")
+    print("|---|---:|---:|" + "---:|" * len(counters) + ("---:|---:|" if "MfmaFlopsBF16" in counters else ""))
+    for key in sorted(vals, key=lambda k: -sum(durs[k].values())):
+        d = list(durs[key].values())
+        us = float(np.median(d))
+        row = f"| `{key[0]}` ({key[1]}) | {len(d)} | {us:.1f} | " + " | ".join(
+            f"{float(np.median(vals[key][c])):.4g}" if vals[key][c] else "" for c in counters)
+        if "MfmaFlopsBF16" in counters:
+            fl = float(np.median(vals[key]["MfmaFlopsBF16"])) if vals[key]["MfmaFlopsBF16"] else 0.0
+            tf = fl / (us * 1e-6) / 1e12 if us > 0 else 0.0
+            row += f" | {tf:.0f} | {tf / 2500:.3f}"
+        print(row + " |")
+
+
 def trace_summary(path: str, warmup: int, steps: int) -> None:
     """Markdown summary of a rocprofv3 kernel trace of a default bench run.
     The timed steps are graph replays W .. W+K-1; a step runs from the first
@@ -205,20 +256,7 @@ def trace_summary(path: str, warmup: int, steps: int) -> None:
                          int(r.get("Grid_Size_Y", 1) or 1)))
     rows.sort()
 
-    def short(n):
-        # "void sd::gemm_kernel<...>(sd::GemmParams) [clone .kd]" -> "sd::gemm_kernel<...>"
-        n = n.split(" [clone")[0].strip()
-        if n.startswith("void "):
-            n = n[5:]
-        if n.endswith(")"):
-            depth = 0
-            for i in range(len(n) - 1, -1, -1):
-                depth += n[i] == ")"
-                depth -= n[i] == "("
-                if depth == 0:
-                    n = n[:i]
-                    break
-        return n
+    short = short_kernel_name
 
     tot = defaultdict(list)
     for s, e, n, *_ in rows:
@@ -295,7 +333,8 @@ def gateup_kernel_name(M: int, N: int) -> str:
                 rows = -(-M // (32 * c)) * 32 * c
                 if rows <= pad:
                     best, pad = c, rows
-        return f"gemm_rows_kernel<{best}, {4 if N % 128 == 0 else 2}, 2>"
+        mtiles = -(-M // (32 * best))
+        return f"gemm_rows_kernel<{best}, {4 if N % 128 == 0 and mtiles * (N // 128) >= 128 else 2}, 2>"
     if M > 64:
         return "gemm_kernel<unsigned short, 4, 2, 2, 2>"
     mt = -(-M // 16)
@@ -570,6 +609,9 @@ def main():
     if args.traffic_from:
         summarise_counters(*args.traffic_from)
         return
+    if args.counters_summary:
+        counters_summary(args.counters_summary)
+        return
     if args.trace_summary:
         trace_summary(args.trace_summary, args.warmup, args.steps)
         return
@@ -621,16 +663,26 @@ def main():
     print(f"[bench] weights on device in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
 
     prompts = synth.prompts(n_tasks, lens, t.vocab)
+
+    def prefill_tasks():
+        # in groups of 16, each reported (slow under counter collection); the
+        # same grouping every time, so that a re-prefill caches the same bits
+        for c in range(0, n_tasks, 16):
+            group = list(range(c, min(c + 16, n_tasks)))
+            eng.prefill(group, [prompts[k] for k in group], [(2 if forced else 1) * max_new] * len(group))
+            print(f"[bench] prefilled tasks {group[0]}..{group[-1]}", file=sys.stderr, flush=True)
+
     t0 = time.time()
-    eng.prefill(list(range(n_tasks)), prompts, [(2 if forced else 1) * max_new] * n_tasks)
+    prefill_tasks()
     print(f"[bench] prefill {n_tasks} tasks, {sum(lens)} tokens in {time.time() - t0:.2f}s", file=sys.stderr,
           flush=True)
 
     batches = [eng.batch(list(range(m * B, (m + 1) * B)), gamma) for m in range(n_batches)]
-    if forced:
+    if forced and not args.pmc_pass:
         # greedy verification emits the target's greedy continuation whatever
         # the drafts, so one unforced run gives each task's continuation; the
         # timed run then starts over with drafts forced to it w.p. alpha
+        # (a counter pass skips it: forcing changes no kernel's shape)
         assert n_batches == 1 and wl.greedy
         t0 = time.time()
         ref = eng.batch(list(range(B)), gamma)
@@ -640,7 +692,7 @@ def main():
         cont = np.array([list(prompts[k]) + em[k][:max_new] for k in range(B)], dtype=np.int32)
         for s_ in range(n_tasks):
             eng.release(s_)
-        eng.prefill(list(range(n_tasks)), prompts, [(2 if forced else 1) * max_new] * n_tasks)
+        prefill_tasks()
         batches[0].set_force(cont, wl.alpha_forced)
         print(f"[bench] reference continuation of {max_new} tokens per task in {time.time() - t0:.1f}s; "
               f"drafts forced with probability {wl.alpha_forced}", file=sys.stderr, flush=True)
