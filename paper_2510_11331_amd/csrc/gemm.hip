@@ -627,8 +627,15 @@ template <typename T, int EPI, int NT, int U>
 static hipError_t launch_mt(int mt, dim3 grid, int threads, const GemmParams& p, hipStream_t s, hipEvent_t e0,
                             hipEvent_t e1) {
   switch (mt) {
-    case 1: launch_k(gemm_kernel<T, 1, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p); break;
-    case 2: launch_k(gemm_kernel<T, 2, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p); break;
+    case 1:
+    case 2:
+      // 96-column tiles (balanced mode) only for 3-tile row blocks
+      if constexpr (NT <= 4) {
+        if (mt == 1) launch_k(gemm_kernel<T, 1, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p);
+        else launch_k(gemm_kernel<T, 2, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p);
+        break;
+      }
+      return hipErrorInvalidValue;
     case 3:
       if constexpr (NT <= 4 || NT == 6) {
         launch_k(gemm_kernel<T, 3, NT, U, EPI>, grid, dim3(threads), 0, s, e0, e1, p);
@@ -673,13 +680,13 @@ bool gemm_config_ok(int dtype, int epi, int nt, int mt, int kw, int grid_x, int 
   const size_t kbytes = (size_t)p.K * (dtype == 0 ? 2 : 4);
   if (mt < 1 || mt > 4 || kw < 1 || kw > 4) return false;
   // instantiated tiles: 48 columns for QKV only, 96 columns (bf16 SwiGLU,
-  // at most 3 row tiles) for balanced mode only
+  // 3 row tiles) for balanced mode only
   switch (nt) {
     case 1: if (epi == EPI_SWIGLU) return false; break;
     case 2: break;
     case 3: if (epi != EPI_QKV || mt > 3) return false; break;
     case 4: if (mt > 3) return false; break;
-    case 6: if (epi != EPI_SWIGLU || dtype != 0 || mt > 3 || p.tile_unit <= 0) return false; break;
+    case 6: if (epi != EPI_SWIGLU || dtype != 0 || mt != 3 || p.tile_unit <= 0) return false; break;
     default: return false;
   }
   if (mt == 4 && nt > 2) return false;
