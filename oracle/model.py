@@ -183,7 +183,8 @@ class Model:
         """Consecutive tokens at positions len(cache)..; same arithmetic as
         repeated decode_row (row i attends to keys 0..its own position), with
         the projections done as one matrix product over the rows.  Appends
-        their K/V; returns logits [n, vocab] (or None)."""
+        their K/V; returns logits [n, vocab] (or None: then the rows' output
+        of the last layer is never used, and only its K/V are computed)."""
         s, w = self.s, self.w
         H, KV, hd = s.n_heads, s.n_kv_heads, s.head_dim
         n = len(tokens)
@@ -197,6 +198,8 @@ class Model:
             k = rope((h @ w[p + "wk"].T).reshape(n, KV, hd), pos, s.rope_theta)
             v = (h @ w[p + "wv"].T).reshape(n, KV, hd)
             cache.append(l, self.r(k), self.r(v))
+            if not logits and l == s.n_layers - 1:
+                return None
             o = np.stack([self.attention(q[i], cache.K[l][:p0 + i + 1], cache.V[l][:p0 + i + 1])
                           for i in range(n)]).reshape(n, -1)
             x = x + self.r(o) @ w[p + "wo"].T

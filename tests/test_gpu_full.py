@@ -16,6 +16,9 @@ are compared with the 2e-2 per-row bound on logits.
   is run whole.
 * The single-task, ragged paged and 13B-width configurations are run on
   layer cuts at their real widths, batch sizes and contexts.
+* The maximum context (32768 positions per slot) is run on a 1-layer cut
+  of the small configuration: 32750 cached positions, so the keys are split
+  12 ways over workgroups and merged.
 """
 import numpy as np
 import pytest
@@ -45,14 +48,14 @@ def _logq_err(q, zr):
     return float(np.abs(e).max() / np.abs(zr).max())
 
 
-def _check(tshape, dshape, tseed, dseed, B, gamma, prompt_len, sample_tasks):
+def _check(tshape, dshape, tseed, dseed, B, gamma, prompt_len, sample_tasks, max_ctx=None):
     """prompt_len: one length, or a list of B lengths (ragged paged batch)."""
     say("full-size parity", tshape, "B", B, "gamma", gamma, "prompt", prompt_len)
     tw, dw = synth.model_weights(tshape, tseed), synth.model_weights(dshape, dseed)
     prompts = synth.prompts(B, prompt_len, tshape.vocab)
     longest = max(len(pr) for pr in prompts)
     eng = make_engine(tshape, dshape, tw, dw, max_slots=B, max_batch=B, gamma_max=gamma,
-                      max_ctx=longest + 2 * (gamma + 1) + 16, prefill_rows=2048)
+                      max_ctx=max_ctx or longest + 2 * (gamma + 1) + 16, prefill_rows=2048)
     slots = list(range(B))
     emitted, acc, b, logits = run_gpu_steps(eng, slots, prompts, gamma, 1, 42, slots, keep_logits=True)
     draft_tok = b.draft_tok.cpu().numpy()
@@ -124,3 +127,11 @@ def test_13b_shape_wide_batch():
     t = synth.MODELS["13b_target"].replace(n_layers=1)
     d = synth.MODELS["13b_draft"].replace(n_layers=1)
     _check(t, d, 1, 2, B=64, gamma=4, prompt_len=512, sample_tasks=[0, 63])
+
+
+def test_small_width_maximum_context():
+    """One task at the largest context a slot takes (max_ctx 32768): a
+    32750-token prompt, gamma = 4, 1-layer cuts of the small GQA pair."""
+    t = synth.MODELS["small_target"].replace(n_layers=1)
+    d = synth.MODELS["small_draft"].replace(n_layers=1)
+    _check(t, d, 1, 2, B=1, gamma=4, prompt_len=32750, sample_tasks=[0], max_ctx=32768)
