@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--sweep-gamma", metavar="GAMMAS", default=None,
                     help="comma-separated speculation lengths: step time, verify / draft latency and tokens per "
                          "step of --workload at each (one JSON line per length), then exit")
+    ap.add_argument("--oracle-timing", action="store_true",
+                    help="the oracle's step time for every configuration on this host, all BLAS threads and one; "
+                         "no GPU; then exit")
     ap.add_argument("--schedule", metavar="FIT_JSON",
                     help="with a runtime fit: plan batches and speculation length for synthetic task sets, "
                          "compare with the baseline policies (predicted), and run plans on the GPU (measured)")
@@ -128,17 +131,19 @@ def summarise_counters(fetch_csv: str, write_csv: str) -> None:
     print(json.dumps(out, indent=1))
 
 
-def cpu_baseline(wl, B, gamma, emitted_per_step):
+def cpu_baseline(wl, B, gamma, emitted_per_step, budget_s=10.0, max_tasks=None):
     """The oracle (float64 NumPy, as it stands) on the host cores, on a
     bounded sample of the workload: the verify pass (forward_rows over
-    gamma+1 rows with 1024 cached positions, LM head included) of every task
-    through a 1-layer and a 2-layer cut of the target, which separates the
-    per-layer cost from the head cost, and gamma draft forwards per task on
-    the full draft.  Scaled to a full step: head + n_layers * layer + drafts."""
+    gamma+1 rows with the workload's cached positions, LM head included) of
+    every task (or of max_tasks of them, scaled to B) through a 1-layer and a
+    2-layer cut of the target, which separates the per-layer cost from the
+    head cost, and gamma draft forwards per task on the full draft.  Scaled to
+    a full step: head + n_layers * layer + drafts."""
     from threadpoolctl import threadpool_info
     from oracle import model as om
     t, d = wl.target, wl.draft
-    ctx = wl.prompt_len
+    ctx = wl.prompt_len or int(np.mean(wl.prompt_range))
+    Bs = min(B, max_tasks or B)                       # tasks timed; the step time is scaled by B / Bs
     two = t.replace(n_layers=2)
     w = synth.model_weights(two, 1)
     m2 = om.Model(two, w)
@@ -157,7 +162,7 @@ def cpu_baseline(wl, B, gamma, emitted_per_step):
 
     def timed_verify(m):
         tot = 0.0
-        for b in range(B):
+        for b in range(Bs):
             c = cache(m, b)
             rows = rng.integers(0, t.vocab, gamma + 1)
             t0 = time.perf_counter()
@@ -167,10 +172,10 @@ def cpu_baseline(wl, B, gamma, emitted_per_step):
 
     # repeat the sample until about 10 s of oracle time has been measured
     reps, t1, t2, td, spent = 0, 0.0, 0.0, 0.0, 0.0
-    while reps == 0 or (spent < 10.0 and reps < 8):
+    while reps == 0 or (spent < budget_s and reps < 8):
         a, b2 = timed_verify(m1), timed_verify(m2)
         dd = 0.0
-        for b in range(B):
+        for b in range(Bs):
             c = cache(md, 100 + b)
             for i in range(gamma):
                 t0 = time.perf_counter()
@@ -178,13 +183,13 @@ def cpu_baseline(wl, B, gamma, emitted_per_step):
                 dd += time.perf_counter() - t0
         t1, t2, td, reps = t1 + a, t2 + b2, td + dd, reps + 1
         spent += a + b2 + dd
-    t1, t2, td = t1 / reps, t2 / reps, td / reps
+    t1, t2, td = t1 / reps * B / Bs, t2 / reps * B / Bs, td / reps * B / Bs
     layer = max(t2 - t1, 0.0)
     head = max(t1 - layer, 0.0)
     t_step = head + t.n_layers * layer + td
     cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": emitted_per_step * B / t_step, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": (f"float64 NumPy oracle, {B} tasks: verify of {gamma + 1} rows with {ctx} cached "
+            "sample": (f"float64 NumPy oracle, {Bs} of {B} tasks: verify of {gamma + 1} rows with {ctx} cached "
                        f"positions through 1- and 2-layer cuts of the {t.n_layers}-layer target (LM head "
                        f"included) and {gamma} draft forwards per task; scaled to a full step = "
                        f"{t_step:.2f} s ({spent:.1f} s sampled over {reps} repetitions)"),
@@ -514,6 +519,25 @@ def schedule_eval(fit_json: str) -> None:
     print(json.dumps(out), flush=True)
 
 
+def oracle_timing() -> None:
+    """The oracle's step time on this host for every configuration, with all
+    BLAS threads and with one (cpu_baseline's sample; up to 8 tasks timed and
+    scaled to the batch).  One JSON line per configuration."""
+    from threadpoolctl import threadpool_limits
+    for name in ("tiny", "small", "7b_b1", "7b_b8", "7b_paged", "13b"):
+        wl = synth.WORKLOADS[name]
+        emitted = 1.0                                  # tokens per task per step scale the rate; report seconds
+        multi = cpu_baseline(wl, wl.batch, wl.gamma, emitted, budget_s=5.0, max_tasks=8)
+        print(f"[oracle] {name}: {multi['step_seconds']} s per step on {multi['cores']} threads", file=sys.stderr,
+              flush=True)
+        with threadpool_limits(limits=1):
+            single = cpu_baseline(wl, wl.batch, wl.gamma, emitted, budget_s=5.0, max_tasks=8)
+        print(json.dumps({"workload": name, "batch": wl.batch, "gamma": wl.gamma,
+                          "step_s_all_threads": multi["step_seconds"], "threads": multi["cores"],
+                          "step_s_one_thread": single["step_seconds"],
+                          "host_cpus": len(os.sched_getaffinity(0)), "sample": multi["sample"]}), flush=True)
+
+
 def gamma_sweep(args) -> None:
     """The speculation-length sweep of a workload (7B B = 1: verify latency
     against gamma; 13B: gamma 2 / 4 / 8): for each gamma a fresh prefill of
@@ -623,6 +647,9 @@ def main():
         return
     if args.sweep_gamma:
         gamma_sweep(args)
+        return
+    if args.oracle_timing:
+        oracle_timing()
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}); "
