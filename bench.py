@@ -131,6 +131,11 @@ def summarise_counters(fetch_csv: str, write_csv: str) -> None:
     print(json.dumps(out, indent=1))
 
 
+def _blas_threads() -> int:
+    from threadpoolctl import threadpool_info
+    return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
+
+
 def cpu_baseline(wl, B, gamma, emitted_per_step, budget_s=10.0, max_tasks=None):
     """The oracle (float64 NumPy, as it stands) on the host cores, on a
     bounded sample of the workload: the verify pass (forward_rows over
@@ -139,7 +144,6 @@ def cpu_baseline(wl, B, gamma, emitted_per_step, budget_s=10.0, max_tasks=None):
     2-layer cut of the target, which separates the per-layer cost from the
     head cost, and gamma draft forwards per task on the full draft.  Scaled to
     a full step: head + n_layers * layer + drafts."""
-    from threadpoolctl import threadpool_info
     from oracle import model as om
     t, d = wl.target, wl.draft
     ctx = wl.prompt_len or int(np.mean(wl.prompt_range))
@@ -187,7 +191,7 @@ def cpu_baseline(wl, B, gamma, emitted_per_step, budget_s=10.0, max_tasks=None):
     layer = max(t2 - t1, 0.0)
     head = max(t1 - layer, 0.0)
     t_step = head + t.n_layers * layer + td
-    cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    cores = _blas_threads()
     return {"value": emitted_per_step * B / t_step, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": (f"float64 NumPy oracle, {Bs} of {B} tasks: verify of {gamma + 1} rows with {ctx} cached "
                        f"positions through 1- and 2-layer cuts of the {t.n_layers}-layer target (LM head "
@@ -519,11 +523,42 @@ def schedule_eval(fit_json: str) -> None:
     print(json.dumps(out), flush=True)
 
 
+def oracle_e2e(name: str) -> dict:
+    """The oracle's speculative decoding of a whole workload, task after task
+    (prefill with batched rows, then SD steps until new_tokens are emitted):
+    verified tokens per second with and without the prefill."""
+    from oracle import model as om, sd as osd
+    wl = synth.WORKLOADS[name]
+    target = om.Model(wl.target, synth.model_weights(wl.target, 1))
+    draft = om.Model(wl.draft, synth.model_weights(wl.draft, 2))
+    prompts = synth.prompts(wl.batch, wl.prompt_len, wl.target.vocab)
+    ut = synth.uniform_table(7, list(range(wl.batch)), wl.new_tokens + 2, wl.gamma)
+    t_pre = t_dec = 0.0
+    tokens = steps = 0
+    for k in range(wl.batch):
+        t0 = time.perf_counter()
+        task = osd.SDTask(target, draft, prompts[k], batch_rows=True)
+        t1 = time.perf_counter()
+        while len(task.emitted) < wl.new_tokens:
+            task.step(wl.gamma, ut[task.n_steps, k], wl.temperature, wl.greedy, batch_rows=True)
+        t2 = time.perf_counter()
+        t_pre, t_dec = t_pre + t1 - t0, t_dec + t2 - t1
+        tokens, steps = tokens + len(task.emitted), steps + task.n_steps
+        print(f"[oracle e2e] {name} task {k}: {task.n_steps} steps, {len(task.emitted)} tokens, "
+              f"prefill {t1 - t0:.2f} s, decode {t2 - t1:.2f} s", file=sys.stderr, flush=True)
+    return {"tokens": tokens, "task_steps": steps, "prefill_s": round(t_pre, 3), "decode_s": round(t_dec, 3),
+            "tokens_per_s_decode": round(tokens / t_dec, 3), "tokens_per_s_with_prefill": round(tokens / (t_pre + t_dec), 3)}
+
+
 def oracle_timing() -> None:
     """The oracle's step time on this host for every configuration, with all
     BLAS threads and with one (cpu_baseline's sample; up to 8 tasks timed and
     scaled to the batch).  One JSON line per configuration."""
     from threadpoolctl import threadpool_limits
+    for name in ("tiny", "small"):
+        r = oracle_e2e(name)
+        print(json.dumps({"workload": name, "end_to_end": r, "threads": _blas_threads(),
+                          "host_cpus": len(os.sched_getaffinity(0))}), flush=True)
     for name in ("tiny", "small", "7b_b1", "7b_b8", "7b_paged", "13b"):
         wl = synth.WORKLOADS[name]
         emitted = 1.0                                  # tokens per task per step scale the rate; report seconds
