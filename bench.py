@@ -343,7 +343,10 @@ def gateup_kernel_name(M: int, N: int) -> str:
                 if rows <= pad:
                     best, pad = c, rows
         mtiles = -(-M // (32 * best))
-        return f"gemm_rows_kernel<{best}, {4 if N % 128 == 0 and mtiles * (N // 128) >= 128 else 2}, 2>"
+        nf = 4 if N % 128 == 0 and mtiles * (N // 128) >= 128 else 2
+        grid = mtiles * N // (32 * nf)
+        nb = (4 if 159 // (4 * best + 4 * nf) >= 4 else 3) if grid <= 256 else 2   # LDS stages
+        return f"gemm_rows_kernel<{best}, {nf}, 2, {nb}>"
     if M > 64:
         return "gemm_kernel<unsigned short, 4, 2, 2, 2>"
     mt = -(-M // 16)

@@ -408,25 +408,43 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
   }
 }
 
+// Wait until at most N vector memory operations of this wave are
+// outstanding (vmcnt only; the LDS and export counters are not waited on).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // Row-tiled GEMM for passes with more than one 64-row block (batched
 // verify at B >= 32, prefill): there every weight byte meets hundreds of
 // rows, so the operands are staged once per workgroup in LDS and shared.
 // A workgroup of 4 waves (2 x 2) owns a BM x BN = 32 MF x 32 NF output tile;
 // wave (wm, wn) owns the 16 MF x 16 NF sub-tile at (wm 16 MF, wn 16 NF).
-// K advances in stages of two k-steps (64 bf16): the 2 (BM + BN) / 16 1 KB
-// fragments of a stage are loaded by the 4 waves into registers while the
-// previous stage is multiplied out of LDS, then written to the other LDS
-// buffer (one barrier per stage).  Rows at or past M load zeros (range-
-// checked buffer loads).  Tile order: the row tiles of one column tile take
-// consecutive slots of one XCD (1-D grid, round-robin dispatch over 8 XCDs),
-// so its weights are fetched from HBM once and re-read from that XCD's L2.
-template <int MF, int NF, int EPI>
+// K advances in stages of two k-steps (64 bf16); a stage is the
+// 2 (BM + BN) / 16 1 KB fragments, which the 4 waves load straight into
+// one of NB LDS buffers (buffer loads with an LDS destination: lane i's
+// 16 bytes land at the buffer's fragment base + 16 i, no registers held).
+// NB - 1 stages are in flight while one is multiplied: at the top of stage
+// st a wave waits until its own loads of stage st have landed (at most
+// NB - 2 stages of its loads outstanding), then one barrier makes every
+// wave's loads visible and frees the buffer stage st - 1 used, which then
+// receives stage st + NB - 1.  Every stage issues the same number of loads
+// (past the last stage, at an out-of-range offset: they read nothing), so
+// the count the wait uses holds to the end.  The barrier is a plain
+// s_barrier with a compiler memory clobber: a fenced one would wait for
+// every load in flight.  Rows at or past M load zeros (range-checked buffer
+// loads).  Tile order: the row tiles of one column tile take consecutive
+// slots of one XCD (1-D grid, round-robin dispatch over 8 XCDs), so its
+// weights are fetched from HBM once and re-read from that XCD's L2.
+template <int MF, int NF, int EPI, int NB>
 __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
   using T = bf16_t;
   constexpr int BM = 32 * MF, BN = 32 * NF;
-  constexpr int FA = 2 * BM / 16, FW = 2 * BN / 16;   // fragments per stage
+  constexpr int FA = 2 * BM / 16, FW = 2 * BN / 16, FS = FA + FW;   // fragments per stage
+  static_assert(NB >= 2 && (NB - 2) * (MF + NF) < 64, "stages in flight");
   extern __shared__ __align__(16) unsigned char smem[];
-  u32x4* lds = (u32x4*)smem;                          // [2][FA + FW][64]
+  u32x4* lds = (u32x4*)smem;                          // [NB][FS][64]
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -451,30 +469,28 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
   const __amdgpu_buffer_rsrc_t ar = buf_rsrc((const char*)p.A + (size_t)bz * (BM / 16) * tile_bytes, (BM / 16) * tile_bytes);
   const int mvalid = p.M - bz * BM;                   // rows of this tile below M
 
-  // this wave's share of a stage: A fragments f = 4 k + wave (k < MF), W
+  // this wave's share of stage st: A fragments f = 4 k + wave (k < MF), W
   // fragments f = 4 k + wave (k < NF); fragment f = 2 t + u is (16-row tile
   // t, k-step u of the stage)
-  u32x4 ra[MF], rw[NF];
   auto gload = [&](int st) {
+    const bool ok = st < stages;
+    u32x4* base = lds + (size_t)(st % NB) * FS * 64;
 #pragma unroll
     for (int k = 0; k < MF; ++k) {
       const int f = 4 * k + wave, t = f >> 1, u = f & 1;
-      const uint32_t off = 16 * t + r16 < mvalid ? ((uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u)
-                                                 : OOB;
-      ra[k] = buf_load16<false>(ar, off);
+      const uint32_t off = ok && 16 * t + r16 < mvalid
+                               ? (uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u
+                               : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ar, (__attribute__((address_space(3))) void*)(base + f * 64), 16, off,
+                                               0, 0, 0);
     }
 #pragma unroll
     for (int k = 0; k < NF; ++k) {
       const int f = 4 * k + wave, t = f >> 1, u = f & 1;
-      rw[k] = buf_load16<false>(wr, (uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u);
+      const uint32_t off = ok ? (uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (__attribute__((address_space(3))) void*)(base + (FA + f) * 64), 16,
+                                               off, 0, 0, 0);
     }
-  };
-  auto lwrite = [&](int buf) {
-    u32x4* base = lds + (size_t)buf * (FA + FW) * 64;
-#pragma unroll
-    for (int k = 0; k < MF; ++k) base[(4 * k + wave) * 64 + lane] = ra[k];
-#pragma unroll
-    for (int k = 0; k < NF; ++k) base[(FA + 4 * k + wave) * 64 + lane] = rw[k];
   };
 
   f32x4 acc[MF][NF];
@@ -483,12 +499,13 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < NF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  gload(0);
-  lwrite(0);
-  __syncthreads();
+#pragma unroll
+  for (int st = 0; st < NB - 1; ++st) gload(st);
   for (int st = 0; st < stages; ++st) {
-    if (st + 1 < stages) gload(st + 1);
-    const u32x4* base = lds + (size_t)(st & 1) * (FA + FW) * 64;
+    wait_vmcnt<(NB - 2) * (MF + NF)>();
+    asm volatile("s_barrier" ::: "memory");
+    gload(st + NB - 1);
+    const u32x4* base = lds + (size_t)(st % NB) * FS * 64;
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       u32x4 a[MF], b[NF];
@@ -501,9 +518,8 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
 #pragma unroll
         for (int j = 0; j < NF; ++j) acc[i][j] = Mfma<T>::step(a[i], b[j], acc[i][j]);
     }
-    if (st + 1 < stages) lwrite((st + 1) & 1);
-    __syncthreads();
   }
+  wait_vmcnt<0>();                                    // the trailing out-of-range loads
 
   // epilogue: element (i, j, v) is row bz BM + wm 16 MF + 16 i + 4 g + v,
   // column n0 + 16 j + r16 with n0 the first column of the wave's sub-tile
@@ -552,27 +568,42 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
     }
 }
 
-size_t gemm_rows_lds(int mf, int nf) { return (size_t)2 * (2 * 32 * mf / 16 + 2 * 32 * nf / 16) * 1024; }
+// LDS stages of the row-tiled GEMM: with one workgroup per CU (at most 256
+// workgroups) as many as fit below 160 KB, up to 4; else 2, so that two
+// workgroups share a CU.  Measured with weights streamed from HBM: 7B
+// gate/up at M = 160 (172 workgroups) 67.7 -> 54.4 us with 4 stages (2:
+// 65.0), QKV 55.3 -> 36.7, LM head 71.9 -> 59.1; 13B gate/up at M = 320
+// (432 workgroups) 118 -> 110 us with 2 stages (4: 124.6), LM head 125.5
+// -> 111.3 (4: 153.8).
+constexpr int rows_stage_kb(int mf, int nf) { return 4 * mf + 4 * nf; }
+constexpr int rows_stages_max(int mf, int nf) { return 159 / rows_stage_kb(mf, nf) >= 4 ? 4 : 3; }
+int gemm_rows_stages(int mf, int nf, int grid) { return grid <= 256 ? rows_stages_max(mf, nf) : 2; }
+size_t gemm_rows_lds(int mf, int nf, int nb) { return (size_t)nb * rows_stage_kb(mf, nf) * 1024; }
 
-template <int EPI, int MF, int NF>
+template <int EPI, int MF, int NF, int NB>
 static hipError_t launch_rows_t(int gz, const GemmParams& p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  const size_t lds = gemm_rows_lds(MF, NF);
+  const size_t lds = gemm_rows_lds(MF, NF, NB);
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_rows_kernel<MF, NF, EPI>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_rows_kernel<MF, NF, EPI, NB>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  launch_k(gemm_rows_kernel<MF, NF, EPI>, dim3(p.N / (32 * NF) * gz), dim3(256), (uint32_t)lds, s, e0, e1, p);
+  launch_k(gemm_rows_kernel<MF, NF, EPI, NB>, dim3(p.N / (32 * NF) * gz), dim3(256), (uint32_t)lds, s, e0, e1, p);
   return hipGetLastError();
 }
 
 template <int EPI>
 static hipError_t launch_rows_e(int mf, int nf, int gz, const GemmParams& p, hipStream_t s, hipEvent_t e0,
                                 hipEvent_t e1) {
-#define SD_ROWS_CASE(MFv, NFv) \
-  if (mf == MFv && nf == NFv) return launch_rows_t<EPI, MFv, NFv>(gz, p, s, e0, e1);
+  const int nb = gemm_rows_stages(mf, nf, p.N / (32 * nf) * gz);
+#define SD_ROWS_CASE(MFv, NFv)                                                            \
+  if (mf == MFv && nf == NFv) {                                                           \
+    constexpr int hi = rows_stages_max(MFv, NFv);                                         \
+    return nb == 2 ? launch_rows_t<EPI, MFv, NFv, 2>(gz, p, s, e0, e1)                    \
+                   : launch_rows_t<EPI, MFv, NFv, hi>(gz, p, s, e0, e1);                  \
+  }
   SD_ROWS_CASE(4, 2) SD_ROWS_CASE(5, 2) SD_ROWS_CASE(6, 2) SD_ROWS_CASE(8, 2)
   SD_ROWS_CASE(4, 4) SD_ROWS_CASE(5, 4) SD_ROWS_CASE(6, 4) SD_ROWS_CASE(8, 4)
 #undef SD_ROWS_CASE

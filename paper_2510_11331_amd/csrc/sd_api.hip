@@ -362,11 +362,17 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
 // tiles for prefill chunks), and 128-column tiles where they leave at least
 // 128 workgroups, else 64-column.  Measured at the 7B B = 32
 // and 13B B = 64 verify shapes (weights streamed from HBM): 13B gate/up at
-// M = 320 108 us against 205 us on the skinny GEMM, LM head 113 against 245.
-// The residual projections (N = d_model) keep the skinny GEMM, which has
-// enough workgroups there (7B O at M = 160: 22 us against 51).  Returns
-// false where the skinny GEMM runs.
+// M = 320 109 us against 205 us on the skinny GEMM, LM head 108 against 245.
+// The residual projections (N = d_model) run on 128 x 64 row tiles from 256
+// to 640 rows (13B B = 64 verify step 23.45 -> 21.78 ms), and on the skinny
+// GEMM below, which has enough workgroups there (7B O at M = 160: 22 us
+// against 33).  Returns false where the skinny GEMM runs.
 bool plan_rows(int M, int N, int dtype, int epi, int* mf, int* nf) {
+  if (epi == EPI_RESID && dtype == SD_DTYPE_BF16 && M >= 256 && M <= 640 && N % 64 == 0) {
+    *mf = 4;
+    *nf = 2;
+    return true;
+  }
   if (dtype != SD_DTYPE_BF16 || M <= GEMM_MROWS || epi == EPI_PART || epi == EPI_RESID || N < 8192) return false;
   int best = 6, pad = 1 << 30;
   if (M <= 640) {
