@@ -291,6 +291,21 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     // rows (i, v) with (4 i + v) % KW == w (for QKV the rows whose
     // positions, KV blocks and rotary inputs it prefetched)
     __shared__ float red[4][MT * NT * 4][64];     // [wave][element][lane]
+    // residual values of this wave's rows, loaded before the reduction (a
+    // load behind the store of the previous row would wait for it)
+    float rres[EPI == EPI_RESID ? MT : 1][4][EPI == EPI_RESID ? NT : 1];
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          if ((4 * i + v) % KW != wave) continue;
+          const int m = m0 + 16 * i + 4 * g + v;
+#pragma unroll
+          for (int j = 0; j < NT; ++j)
+            rres[i][v][j] = m < p.M && j < ntile ? p.out[(size_t)m * p.ldo + n0 + 16 * j + r16] : 0.f;
+        }
+    }
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -345,7 +360,7 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
           for (int j = 0; j < NT; ++j) {
             if (j >= ntile) continue;
             float* dst = p.out + row * p.ldo + n0 + 16 * j + r16;
-            if constexpr (EPI == EPI_RESID) *dst += o[j];
+            if constexpr (EPI == EPI_RESID) *dst = rres[i][v][j] + o[j];
             else *dst = o[j];
           }
         }
@@ -355,6 +370,22 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
     // other waves leave their partial of its tiles in LDS slot
     // (w - f - 1) mod 4
     __shared__ f32x4 red[MT * NT][3][64];           // [tile][slot][lane]
+    // residual values of the units this wave finishes, loaded before the
+    // reduction so that their latency overlaps it
+    float rres[EPI == EPI_RESID ? MT : 1][EPI == EPI_RESID ? UPR : 1][4];
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int k = 0; k < UPR; ++k) {
+          if ((i * UPR + k) % KW != wave || k * TPU >= ntile) continue;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int m = m0 + 16 * i + 4 * g + v;
+            rres[i][k][v] = m < p.M ? p.out[(size_t)m * p.ldo + n0 + 16 * k + r16] : 0.f;
+          }
+        }
+    }
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -400,7 +431,7 @@ __global__ __launch_bounds__((GemmBounds<MT, NT>::threads)) void gemm_kernel(Gem
             if (m >= p.M) continue;
             const size_t row = EPI == EPI_PART ? (size_t)blockIdx.y * p.M + m : (size_t)m;
             float* dst = p.out + row * p.ldo + n0 + 16 * k + r16;
-            if constexpr (EPI == EPI_RESID) *dst += o[v];
+            if constexpr (EPI == EPI_RESID) *dst = rres[i][k][v] + o[v];
             else *dst = o[v];
           }
         }
@@ -522,50 +553,91 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
   wait_vmcnt<0>();                                    // the trailing out-of-range loads
 
   // epilogue: element (i, j, v) is row bz BM + wm 16 MF + 16 i + 4 g + v,
-  // column n0 + 16 j + r16 with n0 the first column of the wave's sub-tile
+  // column n0 + 16 j + r16 with n0 the first column of the wave's sub-tile.
+  // Every load of the epilogue (residual values; row positions, KV blocks
+  // and rotary inputs) is issued for all of the lane's rows before the first
+  // store: a load after a store to a possibly aliasing address would wait
+  // for that store, one round trip per row.
   const int n0 = bx * BN + wn * 16 * NF;
-  int qkind[EPI == EPI_QKV ? NF : 1], qcol[EPI == EPI_QKV ? NF : 1], qf[EPI == EPI_QKV ? NF : 1];
-  size_t qkvb[EPI == EPI_QKV ? NF : 1];
+  const int mrow0 = bz * BM + wm * 16 * MF + 4 * g;    // + 16 i + v
   if constexpr (EPI == EPI_QKV) {
+    int qkind[NF], qcol[NF], qf[NF];
+    size_t qkvb[NF];
 #pragma unroll
     for (int j = 0; j < NF; ++j) qkv_column<T>(p.rope, n0 + 16 * j, r16, qkind[j], qcol[j], qf[j], qkvb[j]);
-  }
+    int pos[MF][4], blk[MF][4];
 #pragma unroll
-  for (int i = 0; i < MF; ++i)
+    for (int i = 0; i < MF; ++i)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int m = bz * BM + wm * 16 * MF + 16 * i + 4 * g + v;
-      float o[NF], pr[EPI == EPI_QKV ? NF : 1];
+      for (int v = 0; v < 4; ++v) {
+        const int m = mrow0 + 16 * i + v;
+        pos[i][v] = m < p.M ? p.rope.row_pos[m] : -1;
+        blk[i][v] = m < p.M ? p.rope.row_blk[m] : -1;
+      }
+    // rotary inputs one 16-row tile ahead of the stores (two register sets)
+    const int half = p.rope.hd / 2;
+    float2 cs[2][4][NF];
+    auto load_cs = [&](int i, float2 (&c)[4][NF]) {
 #pragma unroll
-      for (int j = 0; j < NF; ++j) o[j] = acc[i][j][v];
-      if constexpr (EPI == EPI_QKV) {
+      for (int v = 0; v < 4; ++v)
+#pragma unroll
+        for (int j = 0; j < NF; ++j)
+          c[v][j] = qkind[j] < 2 ? p.rope.tab[(size_t)max(pos[i][v], 0) * half + qf[j]] : float2{1.f, 0.f};
+    };
+    load_cs(0, cs[0]);
+#pragma unroll
+    for (int i = 0; i < MF; ++i) {
+      if (i + 1 < MF) load_cs(i + 1, cs[(i + 1) & 1]);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        float o[NF], pr[NF];
+#pragma unroll
+        for (int j = 0; j < NF; ++j) o[j] = acc[i][j][v];
 #pragma unroll
         for (int j = 0; j < NF; ++j) pr[j] = __shfl_xor(o[j], 8);
+        if (pos[i][v] >= 0)   // a row at or past M has pos -1
+          qkv_store<T, NF>(p.rope, mrow0 + 16 * i + v, pos[i][v], blk[i][v], r16, o, pr, cs[i & 1][v], qkind, qcol,
+                           qkvb);
       }
-      if (m >= p.M) continue;
-      if constexpr (EPI == EPI_QKV) {
-        const int pos = p.rope.row_pos[m];
-        if (pos < 0) continue;
-        const int blk = p.rope.row_blk[m];
-        const int half = p.rope.hd / 2;
-        float2 cs[NF];
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    float r[MF][4][NF];
 #pragma unroll
-        for (int j = 0; j < NF; ++j) cs[j] = qkind[j] < 2 ? p.rope.tab[(size_t)pos * half + qf[j]] : float2{1.f, 0.f};
-        qkv_store<T, NF>(p.rope, m, pos, blk, r16, o, pr, cs, qkind, qcol, qkvb);
-      } else if constexpr (EPI == EPI_SWIGLU) {
-        const int F = p.N / 2;
+    for (int i = 0; i < MF; ++i)
 #pragma unroll
-        for (int j = 0; j < NF; j += 2)
-          Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F), silu(o[j]) * o[j + 1]);
-      } else {
+      for (int v = 0; v < 4; ++v) {
+        const int m = mrow0 + 16 * i + v;
 #pragma unroll
-        for (int j = 0; j < NF; ++j) {
-          float* dst = p.out + (size_t)m * p.ldo + n0 + 16 * j + r16;
-          if constexpr (EPI == EPI_RESID) *dst += o[j];
-          else *dst = o[j];
+        for (int j = 0; j < NF; ++j) r[i][v][j] = m < p.M ? p.out[(size_t)m * p.ldo + n0 + 16 * j + r16] : 0.f;
+      }
+#pragma unroll
+    for (int i = 0; i < MF; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = mrow0 + 16 * i + v;
+        if (m >= p.M) continue;
+#pragma unroll
+        for (int j = 0; j < NF; ++j) p.out[(size_t)m * p.ldo + n0 + 16 * j + r16] = r[i][v][j] + acc[i][j][v];
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < MF; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = mrow0 + 16 * i + v;
+        if (m >= p.M) continue;
+        if constexpr (EPI == EPI_SWIGLU) {
+          const int F = p.N / 2;
+#pragma unroll
+          for (int j = 0; j < NF; j += 2)
+            Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F), silu(acc[i][j][v]) * acc[i][j + 1][v]);
+        } else {
+#pragma unroll
+          for (int j = 0; j < NF; ++j) p.out[(size_t)m * p.ldo + n0 + 16 * j + r16] = acc[i][j][v];
         }
       }
-    }
+  }
 }
 
 // LDS stages of the row-tiled GEMM: with one workgroup per CU (at most 256
