@@ -565,29 +565,8 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
     size_t qkvb[NF];
 #pragma unroll
     for (int j = 0; j < NF; ++j) qkv_column<T>(p.rope, n0 + 16 * j, r16, qkind[j], qcol[j], qf[j], qkvb[j]);
-    int pos[MF][4], blk[MF][4];
-#pragma unroll
-    for (int i = 0; i < MF; ++i)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int m = mrow0 + 16 * i + v;
-        pos[i][v] = m < p.M ? p.rope.row_pos[m] : -1;
-        blk[i][v] = m < p.M ? p.rope.row_blk[m] : -1;
-      }
-    // rotary inputs one 16-row tile ahead of the stores (two register sets)
     const int half = p.rope.hd / 2;
-    float2 cs[2][4][NF];
-    auto load_cs = [&](int i, float2 (&c)[4][NF]) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-#pragma unroll
-        for (int j = 0; j < NF; ++j)
-          c[v][j] = qkind[j] < 2 ? p.rope.tab[(size_t)max(pos[i][v], 0) * half + qf[j]] : float2{1.f, 0.f};
-    };
-    load_cs(0, cs[0]);
-#pragma unroll
-    for (int i = 0; i < MF; ++i) {
-      if (i + 1 < MF) load_cs(i + 1, cs[(i + 1) & 1]);
+    auto store_rows = [&](int i, const int (&pos)[4], const int (&blk)[4], const float2 (&cs)[4][NF]) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         float o[NF], pr[NF];
@@ -595,11 +574,63 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
         for (int j = 0; j < NF; ++j) o[j] = acc[i][j][v];
 #pragma unroll
         for (int j = 0; j < NF; ++j) pr[j] = __shfl_xor(o[j], 8);
-        if (pos[i][v] >= 0)   // a row at or past M has pos -1
-          qkv_store<T, NF>(p.rope, mrow0 + 16 * i + v, pos[i][v], blk[i][v], r16, o, pr, cs[i & 1][v], qkind, qcol,
-                           qkvb);
+        if (pos[v] >= 0)   // a row at or past M has pos -1
+          qkv_store<T, NF>(p.rope, mrow0 + 16 * i + v, pos[v], blk[v], r16, o, pr, cs[v], qkind, qcol, qkvb);
       }
-      __builtin_amdgcn_sched_barrier(0);
+    };
+    auto load_rows = [&](int i, int (&pos)[4], int (&blk)[4]) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = mrow0 + 16 * i + v;
+        pos[v] = m < p.M ? p.rope.row_pos[m] : -1;
+        blk[v] = m < p.M ? p.rope.row_blk[m] : -1;
+      }
+    };
+    auto load_cs = [&](const int (&pos)[4], float2 (&c)[4][NF]) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+#pragma unroll
+        for (int j = 0; j < NF; ++j)
+          c[v][j] = qkind[j] < 2 ? p.rope.tab[(size_t)max(pos[v], 0) * half + qf[j]] : float2{1.f, 0.f};
+    };
+    if constexpr (NB > 2) {
+      // one workgroup per CU: registers to spare, so the positions of all
+      // the lane's rows are loaded at once and the rotary inputs one 16-row
+      // tile ahead of the stores
+      int pos[MF][4], blk[MF][4];
+#pragma unroll
+      for (int i = 0; i < MF; ++i) load_rows(i, pos[i], blk[i]);
+      float2 cs[2][4][NF];
+      load_cs(pos[0], cs[0]);
+#pragma unroll
+      for (int i = 0; i < MF; ++i) {
+        if (i + 1 < MF) load_cs(pos[i + 1], cs[(i + 1) & 1]);
+        store_rows(i, pos[i], blk[i], cs[i & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      // two workgroups per CU (large grids, e.g. prefill): registers are
+      // short, so one row at a time; its loads then wait behind the previous
+      // row's stores, which the long main loop of these shapes hides
+#pragma unroll
+      for (int i = 0; i < MF; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int m = mrow0 + 16 * i + v;
+          float o[NF], pr[NF];
+#pragma unroll
+          for (int j = 0; j < NF; ++j) o[j] = acc[i][j][v];
+#pragma unroll
+          for (int j = 0; j < NF; ++j) pr[j] = __shfl_xor(o[j], 8);
+          if (m >= p.M) continue;
+          const int pos = p.rope.row_pos[m];
+          if (pos < 0) continue;
+          const int blk = p.rope.row_blk[m];
+          float2 cs[NF];
+#pragma unroll
+          for (int j = 0; j < NF; ++j) cs[j] = qkind[j] < 2 ? p.rope.tab[(size_t)pos * half + qf[j]] : float2{1.f, 0.f};
+          qkv_store<T, NF>(p.rope, m, pos, blk, r16, o, pr, cs, qkind, qcol, qkvb);
+        }
     }
   } else if constexpr (EPI == EPI_RESID) {
     float r[MF][4][NF];
