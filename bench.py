@@ -576,13 +576,26 @@ def oracle_timing() -> None:
                           "host_cpus": len(os.sched_getaffinity(0)), "sample": multi["sample"]}), flush=True)
 
 
+def reference_continuation(eng, slots, prompts, gamma, max_new):
+    """Greedy verification emits the target's greedy continuation whatever
+    the drafts: max_new unforced steps of a batch of the given gamma (the
+    timed run's launch configuration, hence its rounding) give each task's
+    continuation, [prompt + max_new tokens] per task."""
+    from paper_2510_11331_amd import generate_graph, emitted_tokens
+    ref = eng.batch(slots, gamma)
+    acc0, out0 = generate_graph(eng, ref, synth.uniform_table(7, slots, max_new, gamma), max_new)
+    em = emitted_tokens(acc0, out0)
+    assert min(len(e) for e in em) >= max_new
+    return np.array([list(prompts[k]) + em[k][:max_new] for k in range(len(slots))], dtype=np.int32)
+
+
 def gamma_sweep(args) -> None:
     """The speculation-length sweep of a workload (7B B = 1: verify latency
     against gamma; 13B: gamma 2 / 4 / 8): for each gamma a fresh prefill of
     the same tasks, W warmup and K timed graph replays of the whole step,
     then the verify pass and the gamma draft calls alone (graph replay, p50)."""
     import torch
-    from paper_2510_11331_amd import SDEngine, StepGraph, generate_graph, emitted_tokens
+    from paper_2510_11331_amd import SDEngine, StepGraph, generate_graph
     wl = synth.WORKLOADS[args.workload]
     gammas = [int(x) for x in args.sweep_gamma.split(",")]
     B, K, W = args.batch or wl.batch, args.steps, args.warmup
@@ -598,17 +611,15 @@ def gamma_sweep(args) -> None:
     tg.close(); dg.close()
     slots = list(range(B))
     prompts = synth.prompts(B, wl.prompt_len, t.vocab)
-    cont = None
-    if forced:
-        eng.prefill(slots, prompts, [2 * max_new] * B)
-        ref = eng.batch(slots, 1)
-        acc0, out0 = generate_graph(eng, ref, synth.uniform_table(7, slots, max_new, 1), max_new)
-        em = emitted_tokens(acc0, out0)
-        cont = np.array([list(prompts[k]) + em[k][:max_new] for k in range(B)], dtype=np.int32)
-        for s_ in slots:
-            eng.release(s_)
     for gamma in gammas:
         eng.prefill(slots, prompts, [2 * max_new] * B)
+        if forced:
+            # the reference runs at the same gamma: the projections' tiling,
+            # and so their rounding, depends on the number of verified rows
+            cont = reference_continuation(eng, slots, prompts, gamma, max_new)
+            for s_ in slots:
+                eng.release(s_)
+            eng.prefill(slots, prompts, [2 * max_new] * B)
         batch = eng.batch(slots, gamma)
         if forced:
             batch.set_force(cont, wl.alpha_forced)
@@ -750,11 +761,7 @@ def main():
         # (a counter pass skips it: forcing changes no kernel's shape)
         assert n_batches == 1 and wl.greedy
         t0 = time.time()
-        ref = eng.batch(list(range(B)), gamma)
-        acc0, out0 = generate_graph(eng, ref, synth.uniform_table(7, list(range(B)), max_new, gamma), max_new)
-        em = emitted_tokens(acc0, out0)
-        assert min(len(e) for e in em) >= max_new
-        cont = np.array([list(prompts[k]) + em[k][:max_new] for k in range(B)], dtype=np.int32)
+        cont = reference_continuation(eng, list(range(B)), prompts, gamma, max_new)
         for s_ in range(n_tasks):
             eng.release(s_)
         prefill_tasks()
