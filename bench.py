@@ -830,9 +830,10 @@ def main():
     gu_bytes = bytes_gu / max(n_gu, 1)
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
     # algorithmic bytes of one verify step: every weight once, the cached K/V
-    # of every task once per layer, the new K/V, logits / probabilities
-    # mean context of batch 0 during the instrumented steps (after W + K steps, K more)
-    P = float(np.mean(lens[:B])) + float((acc + 1).mean()) * (W + 1.5 * K)
+    # of every task once per layer, the new K/V, logits / probabilities; the
+    # verify latency was taken on batch 0 after its W + K steps, so its
+    # context is the prompt plus the tokens those steps committed
+    P = float(np.mean(lens[:B])) + float((acc + 1).mean()) * (W + K)
     kv_bytes = t.n_layers * 2 * t.n_kv_heads * t.head_dim * 2 * B * P
     step_bytes = 2 * t.n_params() + kv_bytes + 2 * B * (gamma + 1) * t.vocab * 4
     verify_p50 = float(np.median(verify_ms))
