@@ -129,6 +129,23 @@ def test_13b_shape_wide_batch():
     _check(t, d, 1, 2, B=64, gamma=4, prompt_len=512, sample_tasks=[0, 63])
 
 
+def test_13b_width_ragged_row_tiles():
+    """13B width, B = 52, gamma = 4: 260 verify rows, so the residual
+    projections run on 128-row tiles whose last one holds 4 rows, and the
+    wide projections on 160-row tiles whose last one holds 100."""
+    t = synth.MODELS["13b_target"].replace(n_layers=1)
+    d = synth.MODELS["13b_draft"].replace(n_layers=1)
+    _check(t, d, 1, 2, B=52, gamma=4, prompt_len=200, sample_tasks=[0, 51])
+
+
+def test_13b_width_largest_row_tiled_residual():
+    """13B width, B = 80, gamma = 7: 640 verify rows, the largest pass whose
+    residual projections run on row tiles."""
+    t = synth.MODELS["13b_target"].replace(n_layers=1)
+    d = synth.MODELS["13b_draft"].replace(n_layers=1)
+    _check(t, d, 1, 2, B=80, gamma=7, prompt_len=96, sample_tasks=[0, 79])
+
+
 def test_small_width_maximum_context():
     """One task at the largest context a slot takes (max_ctx 32768): a
     32750-token prompt, gamma = 4, 1-layer cuts of the small GQA pair."""
