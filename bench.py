@@ -650,6 +650,26 @@ def gamma_sweep(args) -> None:
     eng.close()
 
 
+def copy_ceiling_gbs(nbytes: int = 1 << 30, reps: int = 10) -> float:
+    """HBM rate of a plain device-to-device copy of nbytes (torch's copy
+    kernel), bytes read plus bytes written per second: the practical ceiling
+    a streaming kernel is compared with, beside the 8 TB/s datasheet peak."""
+    import torch
+    src = torch.ones(nbytes // 2, dtype=torch.int16, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2.0 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    return gbs
+
+
 def graph_latencies(eng, batch, u_step, n):
     """Median-ready lists of n replay times (ms) of the verify pass and of the
     gamma draft calls of one batch, each captured as a HIP graph."""
@@ -837,6 +857,7 @@ def main():
     kv_bytes = t.n_layers * 2 * t.n_kv_heads * t.head_dim * 2 * B * P
     step_bytes = 2 * t.n_params() + kv_bytes + 2 * B * (gamma + 1) * t.vocab * 4
     verify_p50 = float(np.median(verify_ms))
+    copy_gbs = copy_ceiling_gbs()
 
     M = B * (gamma + 1)
     gu_name = gateup_kernel_name(M, 2 * t.d_ffn)
@@ -866,6 +887,8 @@ def main():
         "verify_ms_p90": round(float(np.percentile(verify_ms, 90)), 3),
         "verify_hbm_gbs": round(step_bytes / (verify_p50 * 1e-3) / 1e9, 1),
         "verify_hbm_frac": round(step_bytes / (verify_p50 * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "copy_ceiling_gbs": round(copy_gbs, 1),
+        "verify_frac_of_copy": round(step_bytes / (verify_p50 * 1e-3) / 1e9 / copy_gbs, 4),
         "verify_gemm_gbs": round(bytes_all / max(ms_all, 1e-9) * 1e-6, 1),
         "verify_attn_ms_per_layer": round(ms_at / max(n_at, 1), 4),
         "draft_ms_per_call": round(float(np.median(draft_ms)) / gamma, 4),
@@ -878,6 +901,7 @@ def main():
         "roofline": {"kernel": f"{gu_name} (target FFN gate/up, M={M}, N={2 * t.d_ffn}, K={t.d_model})",
                      "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "frac_of_copy": round(achieved / copy_gbs, 4),
                      "traffic": traffic_from_profiles() if headline else None,
                      "launch_ms": round(gu_ms, 5), "algorithmic_bytes_per_launch": gu_bytes},
         "cpu_baseline": None,
