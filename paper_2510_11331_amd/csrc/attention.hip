@@ -377,14 +377,19 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
     __builtin_amdgcn_sched_barrier(0);
   };
   auto step = [&]<int S>(int kb) {
-    f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+    // four independent accumulation chains (the hi and lo parts of q for
+    // each of the two key blocks), so that consecutive matrix instructions
+    // do not wait on each other's results; the parts are added at the end
+    f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = s0, s0l = s0, s1l = s0;
 #pragma unroll
     for (int s = 0; s < UPG; ++s) {
       s0 = mfma_bf16(Kf[S][0][s], qhi[s], s0);
-      s0 = mfma_bf16(Kf[S][0][s], qlo[s], s0);
       s1 = mfma_bf16(Kf[S][1][s], qhi[s], s1);
-      s1 = mfma_bf16(Kf[S][1][s], qlo[s], s1);
+      s0l = mfma_bf16(Kf[S][0][s], qlo[s], s0l);
+      s1l = mfma_bf16(Kf[S][1][s], qlo[s], s1l);
     }
+    s0 += s0l;
+    s1 += s1l;
     float sc[8];
     bool ok[8];
 #pragma unroll
