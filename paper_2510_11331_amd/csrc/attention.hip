@@ -321,7 +321,9 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
     for (int s = 0; s < 2 * UPG; ++s) xv[s] = qs[s];
 #pragma unroll
     for (int s = 0; s < UPG; ++s) {
-      const float sc = qvalid ? p.scale : 0.f;
+      // scores in log2 units (q pre-scaled by log2 e): the softmax then
+      // uses the hardware base-2 exponential
+      const float sc = qvalid ? p.scale * 1.4426950408889634f : 0.f;
       float x[8] = {xv[2 * s].x * sc, xv[2 * s].y * sc, xv[2 * s].z * sc, xv[2 * s].w * sc,
                     xv[2 * s + 1].x * sc, xv[2 * s + 1].y * sc, xv[2 * s + 1].z * sc, xv[2 * s + 1].w * sc};
       split8(x, qhi[s], qlo[s]);
@@ -409,12 +411,12 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
     float pe[8], sum = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      pe[e] = ok[e] ? expf(sc[e] - mnew) : 0.f;
+      pe[e] = ok[e] ? exp2f(sc[e] - mnew) : 0.f;
       sum += pe[e];
     }
     sum += __shfl_xor(sum, 16);
     sum += __shfl_xor(sum, 32);
-    const float alpha = m_run == -INFINITY ? 0.f : expf(m_run - mnew);
+    const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - mnew);
     l_run = l_run * alpha + sum;
     m_run = mnew;
     u32x4 phi, plo;
@@ -467,8 +469,8 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
     if (wave_on && kg % (2 * h) == 0) {
       const float mb = s_m[sl][r16], lb = s_l[sl][r16];
       const float M = fmaxf(m_run, mb);
-      const float a = m_run == -INFINITY ? 0.f : expf(m_run - M);
-      const float b = mb == -INFINITY ? 0.f : expf(mb - M);
+      const float a = m_run == -INFINITY ? 0.f : exp2f(m_run - M);
+      const float b = mb == -INFINITY ? 0.f : exp2f(mb - M);
       l_run = l_run * a + lb * b;
 #pragma unroll
       for (int d = 0; d < DT; ++d)
@@ -503,7 +505,7 @@ __global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p
 #pragma unroll
       for (int v = 0; v < 4; ++v) p.part_o[item * HD + 16 * d + 4 * g + v] = o[d][v];
     if (g == 0) {
-      p.part_ml[item * 2] = m_run;
+      p.part_ml[item * 2] = m_run == -INFINITY ? -INFINITY : m_run * 0.6931471805599453f;   // natural units for the merge
       p.part_ml[item * 2 + 1] = l_run;
     }
   }
