@@ -483,18 +483,24 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
   const int r16 = lane & 15, g = lane >> 4;
   const int ksteps = p.K * 2 / 64, stages = ksteps / 2;
   const int gx = p.N / BN, gz = (p.M + BM - 1) / BM;
-  int bx, bz;
+  // K split: the R = gz ks (row tile, K range) pairs of a column tile take
+  // consecutive slots of one XCD, as the row tiles alone do without a split
+  const int ks = max(p.ksplit, 1), R = gz * ks;
+  int bx, r;
   {
     const int w = blockIdx.x;
     if (gx % 8 == 0) {
       const int j = w >> 3;
-      bz = j % gz;
-      bx = (j / gz) * 8 + (w & 7);
+      r = j % R;
+      bx = (j / R) * 8 + (w & 7);
     } else {
       bx = w % gx;
-      bz = w / gx;
+      r = w / gx;
     }
   }
+  const int bz = r % gz, split = r / gz;
+  const int sps = (stages + ks - 1) / ks;              // stages of one K range
+  const int s_lo = min(split * sps, stages), s_hi = min(s_lo + sps, stages);
   const uint32_t tile_bytes = (uint32_t)ksteps * 1024u;
   const __amdgpu_buffer_rsrc_t wr = buf_rsrc((const char*)p.W + (size_t)bx * (BN / 16) * tile_bytes, (BN / 16) * tile_bytes);
   const __amdgpu_buffer_rsrc_t ar = buf_rsrc((const char*)p.A + (size_t)bz * (BM / 16) * tile_bytes, (BM / 16) * tile_bytes);
@@ -504,7 +510,7 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
   // fragments f = 4 k + wave (k < NF); fragment f = 2 t + u is (16-row tile
   // t, k-step u of the stage)
   auto gload = [&](int st) {
-    const bool ok = st < stages;
+    const bool ok = st < s_hi;
     u32x4* base = lds + (size_t)(st % NB) * FS * 64;
 #pragma unroll
     for (int k = 0; k < MF; ++k) {
@@ -531,8 +537,8 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
     for (int j = 0; j < NF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
-  for (int st = 0; st < NB - 1; ++st) gload(st);
-  for (int st = 0; st < stages; ++st) {
+  for (int st = 0; st < NB - 1; ++st) gload(s_lo + st);
+  for (int st = s_lo; st < s_hi; ++st) {
     wait_vmcnt<(NB - 2) * (MF + NF)>();
     asm volatile("s_barrier" ::: "memory");
     gload(st + NB - 1);
@@ -664,8 +670,9 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
           for (int j = 0; j < NF; j += 2)
             Store<T>::store((T*)p.out_t, Tile<T>::off(m, n0 / 2 + 8 * j + r16, F), silu(acc[i][j][v]) * acc[i][j + 1][v]);
         } else {
+          const size_t row = EPI == EPI_PART ? (size_t)split * p.M + m : (size_t)m;
 #pragma unroll
-          for (int j = 0; j < NF; ++j) p.out[(size_t)m * p.ldo + n0 + 16 * j + r16] = acc[i][j][v];
+          for (int j = 0; j < NF; ++j) p.out[row * p.ldo + n0 + 16 * j + r16] = acc[i][j][v];
         }
       }
   }
@@ -693,14 +700,15 @@ static hipError_t launch_rows_t(int gz, const GemmParams& p, hipStream_t s, hipE
     if (e != hipSuccess) return e;
     attr = true;
   }
-  launch_k(gemm_rows_kernel<MF, NF, EPI, NB>, dim3(p.N / (32 * NF) * gz), dim3(256), (uint32_t)lds, s, e0, e1, p);
+  launch_k(gemm_rows_kernel<MF, NF, EPI, NB>, dim3(p.N / (32 * NF) * gz * std::max(p.ksplit, 1)), dim3(256),
+           (uint32_t)lds, s, e0, e1, p);
   return hipGetLastError();
 }
 
 template <int EPI>
 static hipError_t launch_rows_e(int mf, int nf, int gz, const GemmParams& p, hipStream_t s, hipEvent_t e0,
                                 hipEvent_t e1) {
-  const int nb = gemm_rows_stages(mf, nf, p.N / (32 * nf) * gz);
+  const int nb = gemm_rows_stages(mf, nf, p.N / (32 * nf) * gz * std::max(p.ksplit, 1));
 #define SD_ROWS_CASE(MFv, NFv)                                                            \
   if (mf == MFv && nf == NFv) {                                                           \
     constexpr int hi = rows_stages_max(MFv, NFv);                                         \
@@ -717,11 +725,15 @@ hipError_t launch_gemm_rows(int epi, int mf, int nf, const GemmParams& p, hipStr
                             hipEvent_t e1) {
   const int bn = 32 * nf, bm = 32 * mf;
   if (p.N % bn || p.M < 1 || ((size_t)p.K * 2) % GEMM_CHUNK) return hipErrorInvalidValue;
+  // a K split writes partial sums (PART) and needs at least one stage per range
+  if (p.ksplit > 1 && (epi != EPI_PART || p.ksplit > (int)((size_t)p.K * 2 / GEMM_CHUNK))) return hipErrorInvalidValue;
+  if (epi == EPI_PART && p.ksplit < 1) return hipErrorInvalidValue;
   const int gz = (p.M + bm - 1) / bm;
   switch (epi) {
     case EPI_STORE: return launch_rows_e<EPI_STORE>(mf, nf, gz, p, s, e0, e1);
     case EPI_RESID: return launch_rows_e<EPI_RESID>(mf, nf, gz, p, s, e0, e1);
     case EPI_SWIGLU: return launch_rows_e<EPI_SWIGLU>(mf, nf, gz, p, s, e0, e1);
+    case EPI_PART: return launch_rows_e<EPI_PART>(mf, nf, gz, p, s, e0, e1);
     case EPI_QKV:
       if (p.rope.hd % 16 || p.N != (p.rope.H + 2 * p.rope.KV) * p.rope.hd) return hipErrorInvalidValue;
       return launch_rows_e<EPI_QKV>(mf, nf, gz, p, s, e0, e1);

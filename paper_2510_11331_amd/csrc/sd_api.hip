@@ -190,7 +190,7 @@ void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int q
   ln.q = al.take<float>(sizeof(float) * rows * D.nq);
   ln.att = al.take<void>(D.esz * rows * D.nq);
   ln.hmid = al.take<void>(D.esz * rows * D.F);
-  ln.part_rows = std::min(rows, GEMM_MROWS);
+  ln.part_rows = std::min(rows, 640);   // the largest pass whose residual projections split K
   ln.part = al.take<float>(sizeof(float) * MAX_KSPLIT * ln.part_rows * D.d);
   ln.logits = logits_rows ? al.take<float>(sizeof(float) * logits_rows * D.V) : nullptr;
   ln.attn_items = decode_rb * D.KV;
@@ -363,11 +363,21 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
 // 128 workgroups, else 64-column.  Measured at the 7B B = 32
 // and 13B B = 64 verify shapes (weights streamed from HBM): 13B gate/up at
 // M = 320 109 us against 205 us on the skinny GEMM, LM head 108 against 245.
-// The residual projections (N = d_model) run on 128 x 64 row tiles from 256
-// to 640 rows (13B B = 64 verify step 23.45 -> 21.78 ms), and on the skinny
-// GEMM below, which has enough workgroups there (7B O at M = 160: 22 us
-// against 33).  Returns false where the skinny GEMM runs.
-bool plan_rows(int M, int N, int dtype, int epi, int* mf, int* nf) {
+// The residual projections (N = d_model) from 128 to 640 rows run on
+// 128 x 128 row tiles with K split in 4 when the caller can add partial sums
+// (split_ok; *ks receives the split): 7B at M = 160: O 14.6-15.6 us and down
+// 29.8-32.3 us, against about 22 and 64 on the skinny GEMM; 13B at M = 320:
+// O 24.8 us, down 58.3, against 40.8 and 93.2 unsplit.  Without a split they
+// run on 128 x 64 tiles from 256 to 640 rows and on the skinny GEMM below.
+// Returns false where the skinny GEMM runs.
+bool plan_rows(int M, int N, int dtype, int epi, bool split_ok, int* mf, int* nf, int* ks) {
+  *ks = 1;
+  if (epi == EPI_RESID && dtype == SD_DTYPE_BF16 && split_ok && M >= 128 && M <= 640 && N % 128 == 0) {
+    *mf = 4;
+    *nf = 4;
+    *ks = 4;
+    return true;
+  }
   if (epi == EPI_RESID && dtype == SD_DTYPE_BF16 && M >= 256 && M <= 640 && N % 64 == 0) {
     *mf = 4;
     *nf = 2;
@@ -400,13 +410,16 @@ bool plan_rows(int M, int N, int dtype, int epi, int* mf, int* nf) {
 int gemm(sd_ctx* ctx, const ModelRT& m, int epi, const void* A, const void* W, int M, int N, int K,
          float* out, int ldo, void* out_t, hipStream_t s, int prof_kind, int prof_kind2,
          const RopeParams* rope = nullptr, float* part = nullptr, int* nsplit = nullptr) {
-  GemmPlan g = plan_gemm(M, N, K, m.esz, epi, part != nullptr);
-  if (!g.tu && N % (16 * g.nt)) return SD_EINVAL;
+  int mf = 0, nf = 0, rks = 1;
+  const bool rows = plan_rows(M, N, m.c.dtype, epi, part != nullptr, &mf, &nf, &rks);
+  GemmPlan g = plan_gemm(M, N, K, m.esz, epi, part != nullptr && !rows);
+  if (!rows && !g.tu && N % (16 * g.nt)) return SD_EINVAL;
+  const int ksplit = rows ? rks : g.ksplit;
   if (nsplit) *nsplit = 0;
-  if (g.ksplit > 1) {
+  if (ksplit > 1) {
     epi = EPI_PART;
     out = part;
-    if (nsplit) *nsplit = g.ksplit;
+    if (nsplit) *nsplit = ksplit;
   }
   GemmParams p{};
   p.A = A;
@@ -417,17 +430,17 @@ int gemm(sd_ctx* ctx, const ModelRT& m, int epi, const void* A, const void* W, i
   p.out = out;
   p.ldo = ldo;
   p.out_t = out_t;
-  p.tile_unit = g.tu;
+  p.tile_unit = rows ? 0 : g.tu;
+  p.ksplit = rows ? rks : 0;
   if (rope) p.rope = *rope;
   const double out_bytes = epi == EPI_SWIGLU ? (double)M * (N / 2) * m.esz
                            : epi == EPI_QKV  ? (double)M * (m.nq() * 4 + (N - m.nq()) * m.esz)
-                           : epi == EPI_PART ? (double)M * N * 4 * g.ksplit
+                           : epi == EPI_PART ? (double)M * N * 4 * ksplit
                                              : (double)M * N * 4 * (epi == EPI_RESID ? 2 : 1);
   const double bytes = (double)N * K * m.esz + (double)M * K * m.esz + out_bytes;
   ProfRec r1;
   prof_begin(ctx, s, r1, prof_kind, prof_kind2, bytes, true);
-  int mf = 0, nf = 0;
-  if (plan_rows(M, N, m.c.dtype, epi, &mf, &nf))
+  if (rows)
     HIPCHK(launch_gemm_rows(epi, mf, nf, p, s, r1.a, r1.b));
   else
     HIPCHK(launch_gemm(m.c.dtype == SD_DTYPE_F32 ? 1 : 0, epi, g.nt, g.mt, g.kw, g.gx, g.ksplit, g.gz, p, s, r1.a,

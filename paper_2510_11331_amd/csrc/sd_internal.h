@@ -148,6 +148,8 @@ struct GemmParams {
   RopeParams rope;    // QKV: rotary embedding of q and k, K/V appended to the cache
   int mblocks;        // > 1: 1-D grid of (column tile, M block) pairs, XCD-aware (see gemm.hip)
   int tile_unit;      // > 0: balanced column tiles, dealt in units of tile_unit tiles (see gemm.hip)
+  int ksplit;         // row-tiled GEMM: K in ksplit ranges; with PART, range r's partial sums go to
+                      // out[(r M + m) ldo + n] (0 or 1: no split)
 };
 
 struct AttnParams {
