@@ -258,7 +258,7 @@ __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
 // Lane (r16, g): query r16 of the tile; in S^T it holds keys 4g..4g+3 of
 // both blocks of the step, in O^T dimensions 16 dt + 4g .. +3.
 template <int HD, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void attention_mfma_kernel(AttnParams p) {
+__global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(AttnParams p) {
   constexpr int UPG = HD / 32;             // 16-byte K units per lane group (HD/4 dims)
   constexpr int DT = HD / 16;              // 16-dimension output tiles
   constexpr int NSLOT = WAVES / 2;         // merge slots: half the waves hand over in the first round
@@ -581,11 +581,19 @@ hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEv
   if (dtype == 0) {
     const bool split = p.splits > 1;
     hipEvent_t e1a = split ? nullptr : e1;
+    // four waves per workgroup for large grids (hd 64: 1024 or more
+    // workgroups, hd 128: 2048): two then share a CU, and one's start and
+    // merge overlap the other's stream.  13B B = 64 (2560 verify and 1024
+    // draft workgroups): step 19.73 -> 18.38 ms; 7B paged B = 32 (1024
+    // verify workgroups) is 0.7 % slower with four, so keeps eight
+    const bool many = grid.x * grid.y >= (p.hd == 64 ? 1024u : 2048u);
     if (p.hd == 64) {
-      launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
+      if (many) launch_k(attention_mfma_kernel<64, 4>, grid, dim3(64 * 4), 0, s, e0, e1a, p);
+      else launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
       if (split) launch_k(attn_merge_kernel<bf16_t, 64>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
     } else if (p.hd == 128) {
-      launch_k(attention_mfma_kernel<128, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
+      if (many) launch_k(attention_mfma_kernel<128, 4>, grid, dim3(64 * 4), 0, s, e0, e1a, p);
+      else launch_k(attention_mfma_kernel<128, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
       if (split) launch_k(attn_merge_kernel<bf16_t, 128>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
     } else {
       return hipErrorInvalidValue;
