@@ -15,6 +15,10 @@ Precision (the model definition, shared with the GPU path):
     nearest bf16; keys and values are stored in the cache as bf16.  The
     residual stream, norms, rotary embedding, softmax and all accumulations
     are exact here (float64).
+  * the plain form of a bf16 model (round_activations=False): the same bf16
+    weights and nothing else rounded; every activation and the KV cache stay
+    float64.  This is the unquantised model a bf16 implementation
+    approximates, and the reference for its overall error.
 
 The KV cache is the paper's per-block K^j, V^j, grown by concatenation
 (eq. d_kv) and truncated on rollback.
@@ -44,8 +48,13 @@ def round_bf16(x) -> np.ndarray:
 
 
 def _decode_f64(a: np.ndarray, dtype: str) -> np.ndarray:
+    """bf16 bit patterns (uint16) or float32 values -> float64, exactly: the
+    bf16 pattern is the upper half of the float32 with the same value."""
     if dtype == "bf16":
-        return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+        a = np.ascontiguousarray(a, dtype=np.uint16)
+        f = np.zeros(a.shape + (2,), dtype=np.uint16)
+        f[..., 1] = a                                  # little-endian: high half of each float32
+        return f.view(np.float32).reshape(a.shape).astype(np.float64)
     return np.asarray(a, dtype=np.float32).astype(np.float64)
 
 
@@ -73,6 +82,25 @@ def weights_to_f64(w: Dict[str, np.ndarray], dtype: str) -> Dict[str, np.ndarray
         with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
             list(ex.map(run, jobs))
     return out
+
+
+class LazyF64:
+    """Read-only mapping name -> float64 weight that decodes the stored
+    tensor (bf16 bits or float32) on every access and keeps nothing, so a
+    model whose float64 weights do not fit in memory can be run one layer at
+    a time (Model.sequence_logits reads each tensor once)."""
+
+    def __init__(self, w: Dict[str, np.ndarray], dtype: str):
+        self.src, self.dtype = w, dtype
+
+    def __getitem__(self, name: str) -> np.ndarray:
+        a = self.src[name]
+        if a.ndim == 2 and a.size >= (1 << 22):
+            return weights_to_f64({name: a}, self.dtype)[name]
+        return _decode_f64(a, self.dtype)
+
+    def __contains__(self, name: str) -> bool:
+        return name in self.src
 
 
 def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
@@ -130,13 +158,38 @@ class KVCache:
         return c
 
 
-class Model:
-    """A decoder-only model: shape (synth.ModelShape-like) + float64 weights."""
+def causal_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray, p0: int) -> np.ndarray:
+    """Attention of n consecutive query rows, row i at position p0 + i,
+    each over exactly the keys at positions 0 .. p0 + i (eq. f21 with the
+    causal mask of a decoder): q [n, H, hd], K, V [p0 + n, KV, hd]; query
+    head h reads kv head h // (H / KV); scale 1 / sqrt(hd).  The mask is
+    applied by giving the invisible keys a weight of exactly zero."""
+    n, H, hd = q.shape
+    group = H // K.shape[1]
+    vis = np.arange(K.shape[0])[None, :] <= (p0 + np.arange(n))[:, None]     # [n, keys]
+    out = np.empty((n, H, hd))
+    for h in range(H):
+        s = q[:, h, :] @ K[:, h // group, :].T / math.sqrt(hd)               # [n, keys]
+        s = np.where(vis, s, -np.inf)
+        e = np.exp(s - s.max(axis=1, keepdims=True))
+        out[:, h, :] = (e / e.sum(axis=1, keepdims=True)) @ V[:, h // group, :]
+    return out
 
-    def __init__(self, shape, weights: Dict[str, np.ndarray]):
+
+class Model:
+    """A decoder-only model: shape (synth.ModelShape-like) + float64 weights.
+
+    round_activations (bf16 models only): True applies the bf16 storage
+    points of the model definition above; False gives the plain form (bf16
+    weights, float64 everything else).  lazy=True decodes each weight on
+    access instead of holding all of them in float64 (for models whose
+    float64 weights exceed host memory; use sequence_logits then)."""
+
+    def __init__(self, shape, weights: Dict[str, np.ndarray], round_activations: bool = True,
+                 lazy: bool = False):
         self.s = shape
-        self.w = weights_to_f64(weights, shape.dtype)
-        self.bf16 = shape.dtype == "bf16"
+        self.w = LazyF64(weights, shape.dtype) if lazy else weights_to_f64(weights, shape.dtype)
+        self.bf16 = shape.dtype == "bf16" and round_activations
 
     # storage rounding point of a bf16 model
     def r(self, x: np.ndarray) -> np.ndarray:
@@ -210,6 +263,56 @@ class Model:
             return None
         h = self.r(rmsnorm(x, w["final_norm"], s.rms_eps))
         return h @ w["lm_head"].T
+
+    def unrounded(self) -> "Model":
+        """The plain form of this model (same weights, no activation or KV
+        rounding), sharing the decoded weights."""
+        m = Model.__new__(Model)
+        m.s, m.w, m.bf16 = self.s, self.w, False
+        return m
+
+    def sequence_logits(self, seqs, n_out):
+        """Logits of the last n_out tokens of each sequence of token ids,
+        each sequence starting at position 0 of an empty cache: the rows of
+        all sequences go through one layer at a time (each weight is read
+        once per call), with the attention of every row over exactly the
+        keys of its own sequence up to its own position.  The same arithmetic
+        as prefill + forward_rows, without a cache: keys and values are
+        rounded where the cache would store them.  seqs: a list of token-id
+        sequences (or one sequence); n_out: an int or one per sequence.
+        Returns a list of [n_out, vocab] arrays (one array for one sequence)."""
+        s, w = self.s, self.w
+        H, KV, hd = s.n_heads, s.n_kv_heads, s.head_dim
+        single = len(seqs) > 0 and np.isscalar(seqs[0])
+        seqs = [list(seqs)] if single else [list(q) for q in seqs]
+        outs = [int(n_out)] * len(seqs) if np.isscalar(n_out) else [int(k) for k in n_out]
+        lens = [len(q) for q in seqs]
+        assert all(1 <= o <= n for o, n in zip(outs, lens))
+        starts = np.cumsum([0] + lens)
+        pos = np.concatenate([np.arange(n) for n in lens])
+        x = w["embed"][np.concatenate([np.asarray(q, dtype=np.int64) for q in seqs])]
+        for l in range(s.n_layers):
+            p = f"l{l}."
+            last = l == s.n_layers - 1
+            h = self.r(rmsnorm(x, w[p + "attn_norm"], s.rms_eps))
+            q = rope((h @ w[p + "wq"].T).reshape(-1, H, hd), pos, s.rope_theta)
+            k = self.r(rope((h @ w[p + "wk"].T).reshape(-1, KV, hd), pos, s.rope_theta))
+            v = self.r((h @ w[p + "wv"].T).reshape(-1, KV, hd))
+            o, keep = [], []
+            for i, (a, n) in enumerate(zip(starts[:-1], lens)):
+                m = outs[i] if last else n            # the last layer needs only the output rows
+                o.append(causal_attention(q[a + n - m:a + n], k[a:a + n], v[a:a + n], n - m).reshape(m, -1))
+                keep.append(np.arange(a + n - m, a + n))
+            if last:
+                x = x[np.concatenate(keep)]
+            x = x + self.r(np.concatenate(o)) @ w[p + "wo"].T
+            h = self.r(rmsnorm(x, w[p + "ffn_norm"], s.rms_eps))
+            a_ = silu(h @ w[p + "w_gate"].T) * (h @ w[p + "w_up"].T)
+            x = x + self.r(a_) @ w[p + "w_down"].T
+        h = self.r(rmsnorm(x, w["final_norm"], s.rms_eps))
+        z = h @ w["lm_head"].T
+        res = np.split(z, np.cumsum(outs)[:-1])
+        return res[0] if single else res
 
     def prefill(self, tokens: Sequence[int], batch_rows: bool = False) -> KVCache:
         """Fresh cache holding the K/V of ``tokens`` at positions 0..n-1."""

@@ -206,3 +206,94 @@ def test_table1_shapes_golden():
     assert M["small_target"].d_model == rows["LLaMA-1.1B"][1] and M["small_target"].d_ffn == rows["LLaMA-1.1B"][2]
     # the paper's footprint for LLaMA-7B in FP16 is about 14 GB (Section II)
     assert 13e9 < 2 * M["7b_target"].n_params() < 14.5e9
+
+
+# ---------------------------------------------------------------- plain model, whole-sequence forward
+
+def test_plain_bf16_model_vs_torch_full_forward():
+    """round_activations=False: bf16 weights and nothing else rounded, equal
+    to the independent torch formulation without rounding points."""
+    shape = tiny_shape("bf16", 2)
+    w = synth.model_weights(shape, seed=14)
+    m = om.Model(shape, w, round_activations=False)
+    toks = list(np.random.default_rng(9).integers(0, shape.vocab, 12))
+    c = m.new_cache()
+    got = np.stack([m.decode_row(c, t, i) for i, t in enumerate(toks)])
+    want = torch_reference_logits(shape, m.w, toks)
+    assert np.allclose(got, want, rtol=1e-10, atol=1e-12)
+    # the rounded model differs from it by its storage points only
+    r = om.Model(shape, w)
+    c = r.new_cache()
+    zr = np.stack([r.decode_row(c, t, i) for i, t in enumerate(toks)])
+    assert np.abs(zr - got).max() / np.abs(got).max() > 1e-4
+
+
+def test_causal_attention_vs_torch_sdpa_with_offset():
+    """n query rows at positions p0 .. p0 + n - 1 over p0 + n keys: torch's
+    attention with an explicit mask (key j visible to row i iff j <= p0 + i)."""
+    rng = np.random.default_rng(10)
+    H, KV, hd, p0, n = 4, 2, 16, 7, 5
+    q = rng.standard_normal((n, H, hd))
+    K = rng.standard_normal((p0 + n, KV, hd))
+    V = rng.standard_normal((p0 + n, KV, hd))
+    got = om.causal_attention(q, K, V, p0)
+    mask = torch.arange(p0 + n)[None, :] <= (p0 + torch.arange(n))[:, None]
+    want = F.scaled_dot_product_attention(torch.from_numpy(q).permute(1, 0, 2)[None],
+                                          torch.from_numpy(K).permute(1, 0, 2)[None],
+                                          torch.from_numpy(V).permute(1, 0, 2)[None],
+                                          attn_mask=mask, enable_gqa=True)[0].permute(1, 0, 2)
+    assert np.allclose(got, want.numpy(), rtol=1e-12, atol=1e-13)
+    # one row is the single-query attention of the decoder
+    m = om.Model.__new__(om.Model)
+    m.s = tiny_shape(kv=KV)
+    assert np.allclose(got[2], om.Model.attention(m, q[2], K[:p0 + 3], V[:p0 + 3]), rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("dtype,rounded", [("fp32", True), ("bf16", True), ("bf16", False)])
+def test_sequence_logits_equal_cached_rows(dtype, rounded):
+    """The whole-sequence forward (one layer at a time, lazily decoded
+    weights) gives the logits of prefill + forward_rows, and, for the plain
+    model, those of the torch formulation."""
+    shape = tiny_shape(dtype, 2)
+    w = synth.model_weights(shape, seed=15)
+    toks = list(np.random.default_rng(11).integers(0, shape.vocab, 16))
+    m = om.Model(shape, w, round_activations=rounded)
+    c = m.prefill(toks[:11], batch_rows=True)
+    want = m.forward_rows(c, toks[11:])
+    lazy = om.Model(shape, w, round_activations=rounded, lazy=True)
+    got = lazy.sequence_logits(toks, 5)
+    if dtype == "bf16" and rounded:
+        # a bf16 storage point may flip by one ulp under another summation order
+        assert np.abs(got - want).max() / np.abs(want).max() < 1e-6
+    else:
+        assert np.allclose(got, want, rtol=1e-10, atol=1e-12)
+    if not rounded:
+        assert np.allclose(got, torch_reference_logits(shape, m.w, toks)[11:], rtol=1e-10, atol=1e-12)
+    assert np.allclose(lazy.sequence_logits(toks, 1), got[-1:], rtol=1e-12, atol=1e-13)
+
+
+def test_lazy_weights_decode_like_eager():
+    shape = tiny_shape("bf16", 2)
+    w = synth.model_weights(shape, seed=16)
+    eager = om.weights_to_f64(w, "bf16")
+    lazy = om.LazyF64(w, "bf16")
+    for k in eager:
+        assert np.array_equal(lazy[k], eager[k]), k
+
+
+def test_sequence_logits_of_several_sequences():
+    """Several sequences in one call equal each sequence alone (rows of one
+    sequence never see another's keys), and unrounded() is the plain model."""
+    shape = tiny_shape("bf16", 2)
+    w = synth.model_weights(shape, seed=17)
+    rng = np.random.default_rng(12)
+    seqs = [list(rng.integers(0, shape.vocab, n)) for n in (9, 4, 13)]
+    m = om.Model(shape, w)
+    many = m.sequence_logits(seqs, [3, 4, 1])
+    for sq, o, z in zip(seqs, [3, 4, 1], many):
+        assert z.shape == (o, shape.vocab)
+        alone = m.sequence_logits(sq, o)
+        assert np.abs(z - alone).max() / np.abs(alone).max() < 1e-6
+    plain = om.Model(shape, w, round_activations=False)
+    assert np.allclose(m.unrounded().sequence_logits(seqs[0], 2), plain.sequence_logits(seqs[0], 2),
+                       rtol=1e-12, atol=1e-13)

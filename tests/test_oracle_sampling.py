@@ -185,3 +185,31 @@ def test_expected_emitted_tokens_eq_ol():
     se = emitted.std() / np.sqrt(N)
     assert abs(emitted.mean() - L) < 4 * se, (emitted.mean(), L, se)
     assert 0.3 < alpha < 0.95
+
+
+def test_softmax_f32_hand_example_and_library():
+    """softmax(z / tau): a hand-computed case at tau = 0.5 (exp(z / tau) =
+    1, 2, 3, 4, so p = 0.1 .. 0.4), the same under a shift of 1000 (the
+    maximum is subtracted: exp(2000) would overflow), and torch's softmax of
+    z / tau on random rows at several temperatures.  A z * tau for z / tau,
+    a dropped max-subtraction or a wrong axis fails one of them."""
+    tau = 0.5
+    z = 0.5 * np.log(np.array([1.0, 2.0, 3.0, 4.0]))
+    want = np.array([0.1, 0.2, 0.3, 0.4], dtype=np.float32)
+    got = sp.softmax_f32(z, tau)
+    assert got.dtype == np.float32
+    assert np.array_equal(got, want)
+    assert np.array_equal(sp.softmax_f32(z + 1000.0, tau), want)
+    # two rows at once: normalised over the last axis
+    got2 = sp.softmax_f32(np.stack([z, z[::-1]]), tau)
+    assert np.array_equal(got2, np.stack([want, want[::-1]]))
+    import torch
+    rng = np.random.default_rng(3)
+    for t in (0.1, 0.5, 1.0, 2.0):
+        zz = rng.standard_normal((4, 1000)) * 3.0
+        ref = torch.softmax(torch.from_numpy(zz) / t, dim=-1).to(torch.float32).numpy()
+        # float64 exponentials of two libraries may differ in the last bit,
+        # which can move the float32 result by one unit of its last place
+        got = sp.softmax_f32(zz, t)
+        assert np.all(np.abs(got - ref) <= np.spacing(ref))
+        assert np.allclose(got.sum(axis=-1), 1.0, atol=1e-5)
