@@ -380,6 +380,7 @@ def fit_runtime(out_json: str) -> None:
         for b in bs:
             u = uniforms_device(synth.uniform_table(42, list(range(b)), 1, 8)[0])
             bd = eng.batch(list(range(b)), 2)
+            eng.draft_step(bd, 0, u)                 # the timed call is draft call 1 of a step
             gd = torch.cuda.CUDAGraph()
             with torch.cuda.graph(gd):
                 eng.draft_step(bd, 1, u)
@@ -387,6 +388,8 @@ def fit_runtime(out_json: str) -> None:
             del gd
             for l in ls:
                 bv = eng.batch(list(range(b)), l)
+                for i in range(l):                   # verification follows the step's l draft calls
+                    eng.draft_step(bv, i, u)
                 gv = torch.cuda.CUDAGraph()
                 with torch.cuda.graph(gv):
                     eng.verify(bv)
@@ -677,11 +680,13 @@ def graph_latencies(eng, batch, u_step, n):
     from paper_2510_11331_amd.engine import uniforms_device
     u = uniforms_device(u_step)
     gv, gd = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-    with torch.cuda.graph(gv):
-        eng.verify(batch)
+    # capture order follows the step (draft calls, then verify); capturing
+    # records launches and advances no slot
     with torch.cuda.graph(gd):
         for i in range(batch.gamma):
             eng.draft_step(batch, i, u)
+    with torch.cuda.graph(gv):
+        eng.verify(batch)
     out = []
     for g in (gv, gd):
         g.replay()

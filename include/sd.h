@@ -39,7 +39,25 @@
  *   - Calls that share one context and overlap in time on different streams
  *     must use disjoint slots, and at most one draft call and one
  *     verify/accept/commit sequence may be in flight at a time (they use
- *     separate halves of the workspace).
+ *     separate halves of the workspace).  A context is driven from one host
+ *     thread.
+ *   - Call order.  A batch is the device slot list passed to the step calls
+ *     (identified by its address, with its B and gamma).  Its decoding step
+ *     (Section II-A) is sd_draft_step i = 0 .. gamma-1 in order, then
+ *     sd_verify, then sd_kv_commit; the host checks this order before
+ *     enqueueing and returns SD_ESTATE on a violation:
+ *       draft i = 0   always allowed; starts (or restarts, discarding any
+ *                     uncommitted work of) a step
+ *       draft i > 0   only right after draft i - 1 of the same step
+ *       force i       only after draft i and before draft i + 1 / verify
+ *       verify        only after all gamma drafts of the step; may be
+ *                     repeated (it rewrites the same uncommitted positions)
+ *       commit        only after verify; ends the step (a second commit
+ *                     of the same step is refused)
+ *     sd_accept_resample takes no context and is not tracked: it writes only
+ *     the caller's n_acc / out_tok, which the commit then consumes.
+ *     Capturing calls into a graph performs these checks once, at capture;
+ *     replays repeat the captured order.
  */
 #ifndef SD_H
 #define SD_H
@@ -150,7 +168,12 @@ int sd_init(const sd_config *cfg, const sd_weights *target,
 int sd_prefill(sd_ctx *ctx, int B, const int32_t *slots, const int32_t *tokens,
                const int32_t *lens, const int32_t *max_new, void *stream);
 
-/* Free a slot's KV blocks (host-side; the slot can be prefilled again). */
+/* Free a slot's KV blocks (the slot can be prefilled again).  The slot's
+ * KV capacity on the device is set to 0 with a blocking copy, so a later
+ * pass whose batch still names the slot skips (and flags, see sd_check) its
+ * KV writes instead of writing into blocks handed to another task.  The
+ * caller must not release a slot that queued work still uses.  SD_ESTATE if
+ * the slot is not in use. */
 int sd_release(sd_ctx *ctx, int slot);
 
 /* Drafting, call i of gamma (Section II-A, decoding stage of the draft):
@@ -183,7 +206,9 @@ int sd_verify(sd_ctx *ctx, int B, const int32_t *slots, int gamma,
  * greedy mode draft i is accepted iff it is the arg-max of row i of p (the
  * target logits; lowest index on ties) and the bonus is that arg-max.
  * Writes n_acc[b] = a and out_tok[b, 0..gamma] = t_1..t_a, bonus, then -1.
- * Needs no context: q [B, gamma, vocab], p [B, gamma+1, vocab]. */
+ * Needs no context: q [B, gamma, vocab], p [B, gamma+1, vocab].  Rows are
+ * read as 16-byte vectors: vocab must be a multiple of 4 (4 .. 32768) and q,
+ * p 16-byte aligned; SD_EINVAL otherwise, before anything is enqueued. */
 int sd_accept_resample(int B, int gamma, int vocab, int greedy,
                        const int32_t *draft_tok, const float *q, const float *p,
                        const uint32_t *u, int32_t *n_acc, int32_t *out_tok,

@@ -376,13 +376,13 @@ hipError_t launch_softmax(const SoftmaxParams& p, hipStream_t s) {
 }
 hipError_t launch_draft_sample(const DraftSampleParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  if (p.V > RT * 4 * SV) return hipErrorInvalidValue;
+  if (p.V > RT * 4 * SV || (p.V & 3)) return hipErrorInvalidValue;   // rows are read as float4
   hipLaunchKernelGGL(draft_sample_kernel, dim3(p.B), dim3(RT), 0, s, p);
   return hipGetLastError();
 }
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  if (p.V > RT * 4 * SV) return hipErrorInvalidValue;
+  if (p.V > RT * 4 * SV || (p.V & 3)) return hipErrorInvalidValue;   // rows are read as float4
   hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(RT), 0, s, p);
   return hipGetLastError();
 }

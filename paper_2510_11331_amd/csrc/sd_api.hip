@@ -10,6 +10,7 @@
 #include <cstring>
 #include <deque>
 #include <new>
+#include <unordered_map>
 #include <vector>
 
 namespace sd {
@@ -56,6 +57,15 @@ struct Slot {
   std::vector<int> tblocks, dblocks;
 };
 
+// Where one batch (the device slot list passed to the step calls) stands in
+// its current step: the decoding step of Section II-A is gamma draft calls
+// in order, then verification, then the commit that trims both caches.
+struct Phase {
+  int B = 0, gamma = 0;
+  int drafted = 0;        // draft calls 0 .. drafted-1 of this step are done
+  bool verified = false;  // the verify pass of this step has been enqueued
+};
+
 // One timed interval: either the span of a whole call (events recorded on
 // the stream around it) or one kernel (events stamped by its own dispatch),
 // counted under every kind in the mask.
@@ -77,6 +87,7 @@ struct sd_ctx {
   int keys_per_split = 64, attn_splits = 1;
   std::vector<Slot> slots;
   std::vector<int> free_t, free_d;
+  std::unordered_map<const void*, Phase> phases;   // by device slot-list address
   bool prof = false;
   std::vector<ProfRec> recs;
 };
@@ -585,6 +596,24 @@ bool batch_ok(sd_ctx* ctx, int B, const void* slots, int gamma) {
   return ctx && B >= 1 && B <= ctx->cfg.max_batch && slots && gamma >= 1 && gamma <= ctx->cfg.gamma_max;
 }
 
+// Order of the step calls of one batch (host-side, checked before anything
+// is enqueued).  The batch is identified by its device slot list; a list
+// seen with another B or gamma starts a new record.
+//   draft i = 0      always allowed: starts (or restarts, discarding the
+//                    uncommitted work) a step
+//   draft i > 0      after draft i - 1 of the same step, not after verify
+//   force i          after draft i, before draft i + 1 and verify
+//   verify           after all gamma drafts of the step (may be repeated:
+//                    it rewrites the same uncommitted positions)
+//   commit           after verify; ends the step
+// Acceptance (sd_accept_resample) needs no context and is not tracked: it
+// only writes the caller's n_acc / out_tok, which the commit consumes.
+Phase& phase_of(sd_ctx* ctx, const void* slots, int B, int gamma) {
+  Phase& ph = ctx->phases[slots];
+  if (ph.B != B || ph.gamma != gamma) ph = Phase{B, gamma, 0, false};
+  return ph;
+}
+
 }  // namespace
 
 // ============================================================== C ABI
@@ -776,6 +805,11 @@ int sd_release(sd_ctx* ctx, int slot) {
   if (!ctx || slot < 0 || slot >= ctx->cfg.max_slots) return SD_EINVAL;
   Slot& sl = ctx->slots[slot];
   if (!sl.active) return SD_ESTATE;
+  // capacity 0 on the device: a later pass that still names the slot skips
+  // (and flags) every KV write instead of writing into blocks that another
+  // task may be given next
+  const int32_t zero = 0;
+  HIPCHK(hipMemcpy(ctx->state + (size_t)slot * ST_N + ST_CAP, &zero, sizeof(int32_t), hipMemcpyHostToDevice));
   for (int b : sl.tblocks) ctx->free_t.push_back(b);
   for (int b : sl.dblocks) ctx->free_d.push_back(b);
   sl.tblocks.clear();
@@ -787,6 +821,8 @@ int sd_release(sd_ctx* ctx, int slot) {
 int sd_draft_step(sd_ctx* ctx, int B, const int32_t* slots, int gamma, int i, const uint32_t* u,
                   int32_t* draft_tok, float* q, void* stream) {
   if (!batch_ok(ctx, B, slots, gamma) || i < 0 || i >= gamma || !u || !draft_tok || !q) return SD_EINVAL;
+  Phase& ph = phase_of(ctx, slots, B, gamma);
+  if (i > 0 && (ph.drafted != i || ph.verified)) return SD_ESTATE;
   hipStream_t s = (hipStream_t)stream;
   ModelRT& m = ctx->dft;
   Lane& ln = ctx->ld;
@@ -818,12 +854,16 @@ int sd_draft_step(sd_ctx* ctx, int B, const int32_t* slots, int gamma, int i, co
   dp.greedy = ctx->cfg.greedy;
   HIPCHK(launch_draft_sample(dp, s));
   prof_end(ctx, s, pr);
+  ph.drafted = i + 1;
+  ph.verified = false;
   return SD_OK;
 }
 
 int sd_verify(sd_ctx* ctx, int B, const int32_t* slots, int gamma, const int32_t* draft_tok, float* p,
               float* logits, void* stream) {
   if (!batch_ok(ctx, B, slots, gamma) || !draft_tok || !p) return SD_EINVAL;
+  Phase& ph = phase_of(ctx, slots, B, gamma);
+  if (ph.drafted != gamma) return SD_ESTATE;
   hipStream_t s = (hipStream_t)stream;
   ModelRT& m = ctx->tgt;
   Lane& ln = ctx->lv;
@@ -844,14 +884,17 @@ int sd_verify(sd_ctx* ctx, int B, const int32_t* slots, int gamma, const int32_t
   SoftmaxParams sp{z, p, M, m.c.vocab, 1.0f / ctx->cfg.temperature, ctx->cfg.greedy};
   HIPCHK(launch_softmax(sp, s));
   prof_end(ctx, s, pr);
+  ph.verified = true;
   return SD_OK;
 }
 
 int sd_accept_resample(int B, int gamma, int vocab, int greedy, const int32_t* draft_tok, const float* q,
                        const float* p, const uint32_t* u, int32_t* n_acc, int32_t* out_tok, void* stream) {
-  if (B < 1 || gamma < 1 || gamma > 64 || vocab < 1 || vocab > 32768 || !draft_tok || !q || !p || !u || !n_acc ||
+  if (B < 1 || gamma < 1 || gamma > 64 || vocab < 4 || vocab > 32768 || !draft_tok || !q || !p || !u || !n_acc ||
       !out_tok)
     return SD_EINVAL;
+  // rows of q and p are read as float4: 16-byte aligned starts and whole float4s
+  if ((vocab & 3) || (((uintptr_t)q | (uintptr_t)p) & 15)) return SD_EINVAL;
   AcceptParams ap{};
   ap.B = B;
   ap.gamma = gamma;
@@ -871,8 +914,12 @@ int sd_accept_resample(int B, int gamma, int vocab, int greedy, const int32_t* d
 int sd_kv_commit(sd_ctx* ctx, int B, const int32_t* slots, int gamma, const int32_t* n_acc,
                  const int32_t* out_tok, void* stream) {
   if (!batch_ok(ctx, B, slots, gamma) || !n_acc || !out_tok) return SD_EINVAL;
+  Phase& ph = phase_of(ctx, slots, B, gamma);
+  if (!ph.verified) return SD_ESTATE;
   CommitParams cp{B, gamma, ctx->cfg.max_slots, slots, n_acc, out_tok, ctx->state, ctx->err};
   HIPCHK(launch_commit(cp, (hipStream_t)stream));
+  ph.drafted = 0;
+  ph.verified = false;
   return SD_OK;
 }
 
@@ -882,6 +929,8 @@ int sd_force_draft(sd_ctx* ctx, int B, const int32_t* slots, int gamma, int i, c
       !(alpha >= 0.0 && alpha <= 1.0))
     return SD_EINVAL;
   if (!ctx->cfg.greedy) return SD_ESTATE;   // the draft uniforms are in use when sampling
+  const Phase& ph = phase_of(ctx, slots, B, gamma);
+  if (ph.drafted != i + 1 || ph.verified) return SD_ESTATE;
   ForceParams fp{};
   fp.B = B;
   fp.gamma = gamma;

@@ -53,7 +53,7 @@ def test_sizes_and_validation():
     L = _lib.lib()
     c = make_cfg()
     t = synth.MODELS["tiny_target"]
-    # pool: [layers][blocks][K|V][kv heads][16][head_dim] in the model dtype (fp32 here)
+    # pool: per layer [kv heads][blocks][K|V][16 tokens x head_dim] in the model dtype (fp32 here)
     assert L.sd_kv_pool_bytes(C.byref(c), 0) == t.n_layers * 32 * 2 * t.n_kv_heads * 16 * t.head_dim * 4
     assert L.sd_workspace_bytes(C.byref(c)) > 0
     bad = [dict(kv_block=8), dict(gamma_max=0), dict(gamma_max=17), dict(max_batch=5),
@@ -82,6 +82,15 @@ def test_context_free_and_null_context_errors():
     E = _lib.SD_EINVAL
     assert L.sd_accept_resample(0, 4, 16, 0, None, None, None, None, None, None, None) == E
     assert L.sd_accept_resample(1, 0, 16, 0, 1, 1, 1, 1, 1, 1, None) == E
+    # rows are read as 16-byte vectors: a vocabulary that is not a multiple of
+    # 4, or q / p rows that do not start on 16 bytes, are refused before any
+    # launch (the pointers below are never dereferenced)
+    A = 1 << 20
+    for V in (1, 2, 3, 1001, 31999, 32002):
+        assert L.sd_accept_resample(2, 4, V, 0, A, A, A, A, A, A, None) == E, V
+    assert L.sd_accept_resample(2, 4, 1024, 0, A, A + 8, A, A, A, A, None) == E
+    assert L.sd_accept_resample(2, 4, 1024, 0, A, A, A + 4, A, A, A, None) == E
+    assert L.sd_accept_resample(2, 4, 32772, 0, A, A, A, A, A, A, None) == E
     assert L.sd_draft_step(None, 1, 1, 4, 0, 1, 1, 1, None) == E
     assert L.sd_verify(None, 1, 1, 4, 1, 1, None, None) == E
     assert L.sd_kv_commit(None, 1, 1, 4, 1, 1, None) == E
