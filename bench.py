@@ -69,7 +69,7 @@ def parse():
 
 
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "pmc_traffic.json")
-GATEUP_NAME = "gemm_kernel<unsigned short, 3, 6, 2, 2>"   # bf16 bits, MT=3, NT=6 (balanced), U=2, SwiGLU
+GATEUP_NAME = "gemm_kernel<_Float16, 3, 6, 2, 2>"   # fp16 operands, MT=3, NT=6 (balanced), U=2, SwiGLU
 COPY_NAME = "neg_kernel"                            # torch.neg over 1 GiB of int16
 COPY_BYTES = 1 << 30
 
@@ -152,7 +152,7 @@ def cpu_baseline(wl, B, gamma, emitted_per_step, budget_s=10.0, max_tasks=None):
     w = synth.model_weights(two, 1)
     m2 = om.Model(two, w)
     m1 = om.Model.__new__(om.Model)                   # same float64 weights, first layer only
-    m1.s, m1.w, m1.bf16 = t.replace(n_layers=1), m2.w, m2.bf16
+    m1.s, m1.w, m1.ops, m1.bf16 = t.replace(n_layers=1), m2.w, m2.ops, m2.bf16
     md = om.Model(d, synth.model_weights(d, 2))
     rng = np.random.default_rng(0)
 
@@ -348,13 +348,13 @@ def gateup_kernel_name(M: int, N: int) -> str:
         nb = (4 if 159 // (4 * best + 4 * nf) >= 4 else 3) if grid <= 256 else 2   # LDS stages
         return f"gemm_rows_kernel<{best}, {nf}, 2, {nb}>"
     if M > 64:
-        return "gemm_kernel<unsigned short, 4, 2, 2, 2>"
+        return "gemm_kernel<_Float16, 4, 2, 2, 2>"
     mt = -(-M // 16)
     units = N // 32
     most = -(-units // 256) * 2
     if mt == 3 and units >= 256 and most <= 6:
-        return f"gemm_kernel<unsigned short, 3, {4 if most <= 4 else 6}, 2, 2> (balanced, 256 workgroups)"
-    return f"gemm_kernel<unsigned short, {mt}, {4 if mt == 3 and units < 512 else 2}, 2, 2>"
+        return f"gemm_kernel<_Float16, 3, {4 if most <= 4 else 6}, 2, 2> (balanced, 256 workgroups)"
+    return f"gemm_kernel<_Float16, {mt}, {4 if mt == 3 and units < 512 else 2}, 2, 2>"
 
 
 def fit_runtime(out_json: str) -> None:
@@ -425,7 +425,7 @@ def fit_runtime(out_json: str) -> None:
 
 def schedule_eval(fit_json: str) -> None:
     """The paper's scheduler (libsd sd_sched_*) with the runtime model refit on
-    this GPU.  Predicted: the Section V task set (100 tasks, input lengths
+    this GPU.  Predicted: the Section IV task set (100 tasks, input lengths
     uniform in [1, 512], every task given 2048 output tokens, acceptance rate
     0.8, speculation length up to 10, 16 GB draft memory) under the proposed
     plan (Algorithm 1 + the best speculation length) and the baseline
@@ -826,6 +826,21 @@ def main():
         elapsed = time.perf_counter() - t0
         acc = res_b[0][0]
         emitted = int(sum((a_ + 1).sum() for a_, _ in res_b))
+        # the same tasks from the same state on one stream ("SD w/o pipeline",
+        # Section IV-A): re-prefilled, the same W + K steps with the same
+        # uniforms, so the same trajectory (the streams change no result)
+        for s_ in range(n_tasks):
+            eng.release(s_)
+        prefill_tasks()
+        generate(eng, batches, [u[:W] for u in uts], W, two_streams=False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        res_1 = generate(eng, batches, [u[W:W + K] for u in uts], K, two_streams=False)
+        torch.cuda.synchronize()
+        elapsed_one = time.perf_counter() - t0
+        same = all(np.array_equal(a0, a1) and np.array_equal(o0, o1) for (a0, o0), (a1, o1) in zip(res_b, res_1))
+        print(f"[bench] one stream: {K} steps in {elapsed_one:.3f}s (tokens identical: {same})", file=sys.stderr,
+              flush=True)
     value = emitted / elapsed
     print(f"[bench] timed {K} steps in {elapsed:.3f}s, {emitted} tokens", file=sys.stderr, flush=True)
 
@@ -911,6 +926,25 @@ def main():
                      "launch_ms": round(gu_ms, 5), "algorithmic_bytes_per_launch": gu_bytes},
         "cpu_baseline": None,
     }
+    if n_batches > 1:
+        # two-stream overlap against the same steps on one stream, and the
+        # pipeline latency of eq. time with the measured pass times: per
+        # step, with the paper's per-step barrier (C_{n,0} = 0), M batches
+        # of draft time T_d and verify time T_v take T_d + M T_v when
+        # T_v >= T_d; one stream takes M (T_d + T_v)
+        td_ms, tv_ms = float(np.median(draft_ms)), float(np.median(verify_ms))
+        one_ms, two_ms = elapsed_one / K * 1e3, elapsed / K * 1e3
+        c_d = c_v = 0.0
+        for _ in range(n_batches):
+            c_d += td_ms
+            c_v = max(c_d, c_v) + tv_ms
+        res["pipeline"] = {
+            "two_streams_ms_per_step": round(two_ms, 3), "one_stream_ms_per_step": round(one_ms, 3),
+            "same_tokens": bool(same), "draft_ms_per_batch_step": round(td_ms, 3),
+            "verify_ms_per_batch_step": round(tv_ms, 3),
+            "hidden_draft_fraction": round((one_ms - two_ms) / (n_batches * td_ms), 3),
+            "eq_time_pipelined_ms_per_step": round(c_v, 3),
+            "eq_time_serial_ms_per_step": round(n_batches * (td_ms + tv_ms), 3)}
     if not args.no_cpu_baseline and headline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
         cb = cpu_baseline(wl, B, gamma, float((acc + 1).mean()))

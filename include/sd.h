@@ -84,9 +84,16 @@ enum { SD_DTYPE_BF16 = 0, SD_DTYPE_F32 = 1 };
 /* Decoder-only model (LLaMA layout of the paper's decoder block, eqs. f11,
  * f21, f31): RMSNorm -> QKV -> rotary embedding -> causal attention over the
  * KV cache -> output projection + residual -> RMSNorm -> SwiGLU feed-forward
- * + residual; final RMSNorm and LM head.  dtype is the storage type of the
- * weights and the KV cache; for bf16 every matrix-product input is rounded
- * to bf16, accumulations and the residual stream are fp32. */
+ * + residual; final RMSNorm and LM head.  dtype is the type the weights are
+ * given in.  SD_DTYPE_F32: everything fp32.  SD_DTYPE_BF16: the products run
+ * on fp16 operands with fp32 accumulation: the packed matrices are the fp16
+ * values of the bf16 weights (sd_pack_linear; exact from 2^-14 up, smaller
+ * magnitudes round to the fp16 subnormal grid of 2^-24), every
+ * matrix-product input (normed rows, attention output, SwiGLU output) is
+ * rounded to fp16 and the KV cache holds fp16; embedding rows and norm gains
+ * are read as bf16; the residual stream, norms, rotary embedding and softmax
+ * are fp32.  fp16 has the memory cost and matrix-instruction rate of bf16
+ * and three more significant bits. */
 typedef struct {
     int n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
     int dtype;              /* SD_DTYPE_BF16 or SD_DTYPE_F32                */
@@ -137,10 +144,12 @@ typedef struct {
 } sd_config;
 
 /* Repack a row-major [N, K] matrix of dtype (SD_DTYPE_*) into the layout
- * the matrix-core GEMMs read, enqueued on stream.  The packed matrix has the
- * same size, N K elements.  It is a sequence of 1 KB tiles, tile (n / 16,
- * s) covering rows 16 (n/16) .. +15 and the s-th 64-byte run of those rows'
- * K extent (E = 32 bf16 or 16 fp32 elements); tiles are ordered row block
+ * the matrix-core GEMMs read, enqueued on stream; a bf16 matrix is written
+ * as fp16 (each value rounded to nearest even: exact from 2^-14 up).  The
+ * packed matrix has the same size, N K elements.  It is a sequence of 1 KB
+ * tiles, tile (n / 16, s) covering rows 16 (n/16) .. +15 and the s-th
+ * 64-byte run of those rows' K extent (E = 32 fp16 or 16 fp32 elements);
+ * tiles are ordered row block
  * major.  Inside a tile, element (n, k) with k = s E + e sits in 16-byte
  * unit 16 (e / (E/4)) + n % 16 at position e % (E/4): one wave-wide 16-byte
  * load per lane fetches a tile whole.  Requirements: N % 16 == 0 and

@@ -6,10 +6,10 @@
  * sd.h (SD_OK, SD_EINVAL for bad arguments, SD_ENOMEM when the draft memory
  * budget admits no batching).  Outputs are written only on SD_OK.
  *
- * The model is the paper's (Section III, "Inference Cost Model" and
+ * The model is the paper's (Sections II-C "Inference Cost Model" and II-D
  * "Serving Latency Model"):
  *   - a task k has input length I_k; every task is given O_max output
- *     tokens (the simplification of Section IV-B, so every batch runs every
+ *     tokens (the simplification of Section III-B, so every batch runs every
  *     step); a batch m of b_m tasks has I_m = max of its input lengths;
  *   - tokens emitted per step L = (1 - alpha^(l+1)) / (1 - alpha) (eq. ol;
  *     l + 1 at alpha = 1) and steps N = ceil(O_max / L) (eq. step_n);
@@ -67,7 +67,7 @@ typedef struct {
 int sd_sched_latency(const sd_sched_cfg *cfg, int K, const int32_t *input_len, int n_batches,
                      const int32_t *batch_of, int l, double *t_inf);
 
-/* Batching for a given speculation length l (Section IV-B, Algorithm 1).
+/* Batching for a given speculation length l (Section III-B, Algorithm 1).
  * Tasks are sorted by input length (ties by index); a batch is a run of the
  * sorted order.  Dynamic program over the sorted prefix: Y[i][n] = (first-
  * stage, second-stage) completion at step n of the plan chosen for the
@@ -82,14 +82,14 @@ int sd_sched_latency(const sd_sched_cfg *cfg, int K, const int32_t *input_len, i
 int sd_sched_batching(const sd_sched_cfg *cfg, int K, const int32_t *input_len, int l, int32_t *batch_of,
                       int *n_batches, double *t_inf);
 
-/* Speculation length (Section IV-B, problem P3): the batching of
+/* Speculation length (Section III-B, problem P3): the batching of
  * sd_sched_batching for every l in 1..l_max, keeping the lowest T_inf (ties
  * to the smaller l).  Outputs as sd_sched_batching plus *l_best and, if
  * t_inf_by_l is not null, T_inf of every l in t_inf_by_l[l_max]. */
 int sd_sched_plan(const sd_sched_cfg *cfg, int K, const int32_t *input_len, int l_max, int32_t *batch_of,
                   int *n_batches, int *l_best, double *t_inf, double *t_inf_by_l);
 
-/* Uplink bandwidth shares (Section IV-A, eq. opt_w): w_k proportional to
+/* Uplink bandwidth shares (Section III-A, eq. opt_w): w_k proportional to
  * I_k / log2(1 + snr_k) with sum w_k = 1, so that every upload of
  * lambda_bits I_k bits over w_k bandwidth_hz finishes at the same time
  * *t_com = sum_k lambda_bits I_k / (bandwidth_hz log2(1 + snr_k)).

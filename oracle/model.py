@@ -10,14 +10,18 @@ grouped KV heads.  d0 is the head dimension.
 
 Precision (the model definition, shared with the GPU path):
   * fp32 models: no storage rounding anywhere.
-  * bf16 models: weights are bf16; every matrix-product input (the normed
-    activations, the attention output, the SwiGLU output) is rounded to the
-    nearest bf16; keys and values are stored in the cache as bf16.  The
-    residual stream, norms, rotary embedding, softmax and all accumulations
-    are exact here (float64).
-  * the plain form of a bf16 model (round_activations=False): the same bf16
-    weights and nothing else rounded; every activation and the KV cache stay
-    float64.  This is the unquantised model a bf16 implementation
+  * bf16 models: the weights are bf16 values.  The products take their
+    operands in IEEE fp16: the projection matrices and the LM head enter as
+    the nearest fp16 of each bf16 weight (the same value from 2^-14 up;
+    smaller magnitudes round to fp16's subnormal grid of 2^-24); every
+    matrix-product input (the normed activations, the attention output, the
+    SwiGLU output) is rounded to the nearest fp16; keys and values are stored
+    in the cache as fp16.  The embedding rows and norm gains are used as bf16
+    values.  The residual stream, norms, rotary embedding, softmax and all
+    accumulations are exact here (float64).
+  * the plain form of a bf16 model (round_activations=False): the bf16
+    weights as they are and nothing else rounded; every activation and the
+    KV cache stay float64.  This is the unquantised model an implementation
     approximates, and the reference for its overall error.
 
 The KV cache is the paper's per-block K^j, V^j, grown by concatenation
@@ -47,57 +51,49 @@ def round_bf16(x) -> np.ndarray:
     return a
 
 
+def round_fp16(x) -> np.ndarray:
+    """Nearest IEEE fp16 value (ties to even, subnormals kept) of float64
+    data, returned as float64 (numpy converts float64 to float16 directly,
+    with one rounding)."""
+    return np.asarray(x, dtype=np.float64).astype(np.float16).astype(np.float64)
+
+
+# the weights a product reads (the projection matrices and the LM head)
+_MATRICES = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
+
+
+def is_matrix(name: str) -> bool:
+    return name == "lm_head" or name.split(".")[-1] in _MATRICES
+
+
 def _decode_f64(a: np.ndarray, dtype: str) -> np.ndarray:
-    """bf16 bit patterns (uint16) or float32 values -> float64, exactly: the
-    bf16 pattern is the upper half of the float32 with the same value."""
+    """bf16 bit patterns (uint16) or float32 values -> float64, exactly (a
+    plain dtype conversion; torch's is used for bf16, which numpy lacks)."""
     if dtype == "bf16":
-        a = np.ascontiguousarray(a, dtype=np.uint16)
-        f = np.zeros(a.shape + (2,), dtype=np.uint16)
-        f[..., 1] = a                                  # little-endian: high half of each float32
-        return f.view(np.float32).reshape(a.shape).astype(np.float64)
+        import torch
+        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint16).view(np.int16)).view(torch.bfloat16)
+        return t.to(torch.float64).numpy()
     return np.asarray(a, dtype=np.float32).astype(np.float64)
 
 
 def weights_to_f64(w: Dict[str, np.ndarray], dtype: str) -> Dict[str, np.ndarray]:
-    """Decode stored weights (bf16 bit patterns or float32) into float64
-    (exact; large tensors are decoded in row chunks on a thread pool)."""
-    import os
-    from concurrent.futures import ThreadPoolExecutor
-    out = {}
-    jobs = []
-    for k, a in w.items():
-        if a.ndim == 2 and a.size >= (1 << 22):
-            o = np.empty(a.shape, dtype=np.float64)
-            out[k] = o
-            step = max(1, (1 << 21) // a.shape[1])
-            jobs += [(a, o, r, min(r + step, a.shape[0])) for r in range(0, a.shape[0], step)]
-        else:
-            out[k] = _decode_f64(a, dtype)
-
-    def run(job):
-        a, o, r0, r1 = job
-        o[r0:r1] = _decode_f64(a[r0:r1], dtype)
-
-    if jobs:
-        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
-            list(ex.map(run, jobs))
-    return out
+    """Decode stored weights (bf16 bit patterns or float32) into float64 (exact)."""
+    return {k: _decode_f64(a, dtype) for k, a in w.items()}
 
 
 class LazyF64:
     """Read-only mapping name -> float64 weight that decodes the stored
     tensor (bf16 bits or float32) on every access and keeps nothing, so a
     model whose float64 weights do not fit in memory can be run one layer at
-    a time (Model.sequence_logits reads each tensor once)."""
+    a time (Model.sequence_logits reads each tensor once).  operands=True
+    gives the matrices as the products read them (round_fp16)."""
 
-    def __init__(self, w: Dict[str, np.ndarray], dtype: str):
-        self.src, self.dtype = w, dtype
+    def __init__(self, w: Dict[str, np.ndarray], dtype: str, operands: bool = False):
+        self.src, self.dtype, self.operands = w, dtype, operands
 
     def __getitem__(self, name: str) -> np.ndarray:
-        a = self.src[name]
-        if a.ndim == 2 and a.size >= (1 << 22):
-            return weights_to_f64({name: a}, self.dtype)[name]
-        return _decode_f64(a, self.dtype)
+        a = _decode_f64(self.src[name], self.dtype)
+        return round_fp16(a) if self.operands and is_matrix(name) else a
 
     def __contains__(self, name: str) -> bool:
         return name in self.src
@@ -188,12 +184,18 @@ class Model:
     def __init__(self, shape, weights: Dict[str, np.ndarray], round_activations: bool = True,
                  lazy: bool = False):
         self.s = shape
-        self.w = LazyF64(weights, shape.dtype) if lazy else weights_to_f64(weights, shape.dtype)
         self.bf16 = shape.dtype == "bf16" and round_activations
+        if lazy:
+            self.w = LazyF64(weights, shape.dtype)
+            self.ops = LazyF64(weights, shape.dtype, operands=self.bf16)
+        else:
+            self.w = weights_to_f64(weights, shape.dtype)
+            self.ops = ({k: round_fp16(v) if is_matrix(k) else v for k, v in self.w.items()} if self.bf16
+                        else self.w)
 
-    # storage rounding point of a bf16 model
+    # storage rounding point of a bf16 model: an fp16 operand
     def r(self, x: np.ndarray) -> np.ndarray:
-        return round_bf16(x) if self.bf16 else x
+        return round_fp16(x) if self.bf16 else x
 
     def new_cache(self) -> KVCache:
         return KVCache(self.s.n_layers, self.s.n_kv_heads, self.s.head_dim)
@@ -213,7 +215,7 @@ class Model:
     def decode_row(self, cache: KVCache, token: int, pos: int) -> np.ndarray:
         """Process one token at absolute position pos == len(cache); appends
         its K/V to the cache and returns its next-token logits [vocab]."""
-        s, w = self.s, self.w
+        s, w = self.s, self.ops
         assert pos == len(cache), (pos, len(cache))
         H, KV, hd = s.n_heads, s.n_kv_heads, s.head_dim
         x = w["embed"][int(token)].copy()
@@ -238,7 +240,7 @@ class Model:
         the projections done as one matrix product over the rows.  Appends
         their K/V; returns logits [n, vocab] (or None: then the rows' output
         of the last layer is never used, and only its K/V are computed)."""
-        s, w = self.s, self.w
+        s, w = self.s, self.ops
         H, KV, hd = s.n_heads, s.n_kv_heads, s.head_dim
         n = len(tokens)
         p0 = len(cache)
@@ -268,7 +270,7 @@ class Model:
         """The plain form of this model (same weights, no activation or KV
         rounding), sharing the decoded weights."""
         m = Model.__new__(Model)
-        m.s, m.w, m.bf16 = self.s, self.w, False
+        m.s, m.w, m.ops, m.bf16 = self.s, self.w, self.w, False
         return m
 
     def sequence_logits(self, seqs, n_out):
@@ -281,7 +283,7 @@ class Model:
         rounded where the cache would store them.  seqs: a list of token-id
         sequences (or one sequence); n_out: an int or one per sequence.
         Returns a list of [n_out, vocab] arrays (one array for one sequence)."""
-        s, w = self.s, self.w
+        s, w = self.s, self.ops
         H, KV, hd = s.n_heads, s.n_kv_heads, s.head_dim
         single = len(seqs) > 0 and np.isscalar(seqs[0])
         seqs = [list(seqs)] if single else [list(q) for q in seqs]

@@ -1,8 +1,8 @@
 """Oracle of the paper's serving scheduler (test infrastructure only).
 
-Written from Section III ("Inference Cost Model", "Serving Latency Model")
-and Section IV ("Optimal Communication Resource Allocation", "Optimal
-Batching and Speculation Length", Algorithm 1) of the paper, in float64,
+Written from Sections II-C and II-D ("Inference Cost Model", "Serving
+Latency Model") and Sections III-A and III-B ("Optimal Communication Resource
+Allocation", "Optimal Batching and Speculation Length", Algorithm 1) of the paper, in float64,
 with plain loops.  It shares no code with the scheduler in the HIP library.
 
 Model (per task k: input length I_k; per batch m: I_m = max input length,

@@ -6,12 +6,12 @@
 // Paged layout of one layer's pool: head-major tiles [kv head][block][K|V]
 // (kv_tile_off), so that the blocks of one task and head, allocated in
 // order, are one contiguous run; K in the layout of the S = K Q^T matrix
-// instruction for bf16 (kv_key_off: every wave load of a key k-step is a
-// contiguous 1 KB) or as [16 tokens][hd] for fp32; V transposed so that the
-// P*V operand of a matrix instruction is 4 consecutive tokens of one
-// dimension (kv_val_off: for bf16 two such quads per 16-byte unit, 1 KB per
-// wave load; [hd][16 tokens] for fp32); a slot's block table maps position /
-// 16 to a block.
+// instruction for 16-bit caches (kv_key_off: every wave load of a key k-step
+// is a contiguous 1 KB) or as [16 tokens][hd] for fp32; V transposed so that
+// the P*V operand of a matrix instruction is 4 consecutive tokens of one
+// dimension (kv_val_off: for 16-bit caches two such quads per 16-byte unit,
+// 1 KB per wave load; [hd][16 tokens] for fp32); a slot's block table maps
+// position / 16 to a block.
 //
 // Attention work item = (row block, kv head, key split).  A row block is a
 // run of consecutive rows of one task (the gamma+1 verify rows of a task, its
@@ -22,19 +22,20 @@
 // when the keys are split, partial (max, sum, output) triples go to a
 // workspace and a second kernel merges them in split order.
 //
-// bf16 models: S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_16x16x32_bf16,
-// 16 query vectors per wave, keys streamed from the cache straight into
-// registers 32 at a time (two blocks), one step ahead, with non-temporal
-// loads (each cache byte is read once per pass); q and p enter the
-// matrix instruction as bf16 hi + lo pairs, which keeps them at ~2^-16
-// relative precision.  fp32 models: a vector kernel with K/V staged in LDS.
+// bf16 models (fp16 KV cache, see f16_t): S^T = K Q^T and O^T += V^T P^T on
+// v_mfma_f32_16x16x32_f16, 16 query vectors per wave, keys streamed from the
+// cache straight into registers 32 at a time (two blocks), one step ahead,
+// with non-temporal loads (each cache byte is read once per pass); q and p
+// enter the matrix instruction as fp16 hi + lo pairs, which keeps them at
+// ~2^-22 relative precision.  fp32 models: a vector kernel with K/V staged
+// in LDS.
 #include "sd_internal.h"
 
 #include <algorithm>
 
 namespace sd {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -63,7 +64,7 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// the vector kernel serves fp32 caches only (bf16 runs on the matrix kernel)
+// the vector kernel serves fp32 caches only (16-bit caches run on the matrix kernel)
 template <typename T> struct KvT;
 template <> struct KvT<float> {
   static constexpr int KST_PAD = 1;
@@ -234,13 +235,14 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
   }
 }
 
-// bf16 hi + lo pair of 8 floats, packed as two bf16x8 operands
+// fp16 hi + lo pair of 8 floats (hi = x rounded, lo = the rest rounded),
+// packed as two f16x8 operands
 __device__ __forceinline__ void split8(const float (&x)[8], u32x4& hi, u32x4& lo) {
   uint32_t h[4], l[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const bf16_t a0 = f2bf(x[2 * k]), a1 = f2bf(x[2 * k + 1]);
-    const bf16_t b0 = f2bf(x[2 * k] - bf2f(a0)), b1 = f2bf(x[2 * k + 1] - bf2f(a1));
+    const uint16_t a0 = f2h(x[2 * k]), a1 = f2h(x[2 * k + 1]);
+    const uint16_t b0 = f2h(x[2 * k] - h2f(a0)), b1 = f2h(x[2 * k + 1] - h2f(a1));
     h[k] = (uint32_t)a0 | ((uint32_t)a1 << 16);
     l[k] = (uint32_t)b0 | ((uint32_t)b1 << 16);
   }
@@ -248,9 +250,9 @@ __device__ __forceinline__ void split8(const float (&x)[8], u32x4& hi, u32x4& lo
   lo = u32x4{l[0], l[1], l[2], l[3]};
 }
 
-__device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
-                                                 c, 0, 0, 0);
+__device__ __forceinline__ f32x4 mfma_f16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                0, 0);
 }
 
 // Wave w of a workgroup (WAVES = 8) takes query tile w % QTe (16 query
@@ -336,11 +338,11 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(A
   for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // this kv head's region of the pool ([blocks][K|V][16 x HD], 2 x 16 HD
-  // bf16 per block) as a range-checked buffer: steps past the key range
+  // fp16 per block) as a range-checked buffer: steps past the key range
   // load at an out-of-range offset, which returns zero and reads nothing
   constexpr uint32_t BLK_BYTES = 2u * 16u * HD * 2u;
   const __amdgpu_buffer_rsrc_t kvr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<bf16_t*>((const bf16_t*)p.kv + kv_tile_off(kvh, 0, 0, p.nblk, HD)), (short)0,
+      const_cast<f16_t*>((const f16_t*)p.kv + kv_tile_off(kvh, 0, 0, p.nblk, HD)), (short)0,
       (int)((uint32_t)p.nblk * BLK_BYTES), 0x00020000);
   // key tile in the matrix-instruction layout: k-step s is the 1 KB run at
   // unit 64 s, this lane's 16 bytes at unit 64 s + lane (token r16, dims
@@ -385,10 +387,10 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(A
     f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = s0, s0l = s0, s1l = s0;
 #pragma unroll
     for (int s = 0; s < UPG; ++s) {
-      s0 = mfma_bf16(Kf[S][0][s], qhi[s], s0);
-      s1 = mfma_bf16(Kf[S][1][s], qhi[s], s1);
-      s0l = mfma_bf16(Kf[S][0][s], qlo[s], s0l);
-      s1l = mfma_bf16(Kf[S][1][s], qlo[s], s1l);
+      s0 = mfma_f16(Kf[S][0][s], qhi[s], s0);
+      s1 = mfma_f16(Kf[S][1][s], qhi[s], s1);
+      s0l = mfma_f16(Kf[S][0][s], qlo[s], s0l);
+      s1l = mfma_f16(Kf[S][1][s], qlo[s], s1l);
     }
     s0 += s0l;
     s1 += s1l;
@@ -428,8 +430,8 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(A
       const u32x4 v0 = Vr[S][0][d / 2], v1 = Vr[S][1][d / 2];
       const u32x4 va = (d & 1) ? u32x4{v0.z & Vm[S][0][0], v0.w & Vm[S][0][1], v1.z & Vm[S][1][0], v1.w & Vm[S][1][1]}
                                : u32x4{v0.x & Vm[S][0][0], v0.y & Vm[S][0][1], v1.x & Vm[S][1][0], v1.y & Vm[S][1][1]};
-      o[d] = mfma_bf16(va, phi, o[d]);
-      o[d] = mfma_bf16(va, plo, o[d]);
+      o[d] = mfma_f16(va, phi, o[d]);
+      o[d] = mfma_f16(va, plo, o[d]);
     }
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -483,9 +485,9 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(A
   const bool owner = wave_on && kg == 0 && qvalid;
   // four consecutive output dimensions of this lane's query, MFMA-tile layout
   auto emit4 = [&](int d, float a0, float a1, float a2, float a3) {
-    const size_t off = Tile<bf16_t>::off(qrow, qh * HD + 16 * d + 4 * g, p.H * HD);
-    *(uint2*)((bf16_t*)p.out + off) = make_uint2((uint32_t)f2bf(a0) | ((uint32_t)f2bf(a1) << 16),
-                                                 (uint32_t)f2bf(a2) | ((uint32_t)f2bf(a3) << 16));
+    const size_t off = Tile<f16_t>::off(qrow, qh * HD + 16 * d + 4 * g, p.H * HD);
+    *(uint2*)((f16_t*)p.out + off) = make_uint2((uint32_t)f2h(a0) | ((uint32_t)f2h(a1) << 16),
+                                                (uint32_t)f2h(a2) | ((uint32_t)f2h(a3) << 16));
   };
 
   if (p.splits == 1) {
@@ -590,11 +592,11 @@ hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEv
     if (p.hd == 64) {
       if (many) launch_k(attention_mfma_kernel<64, 4>, grid, dim3(64 * 4), 0, s, e0, e1a, p);
       else launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
-      if (split) launch_k(attn_merge_kernel<bf16_t, 64>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
+      if (split) launch_k(attn_merge_kernel<f16_t, 64>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
     } else if (p.hd == 128) {
       if (many) launch_k(attention_mfma_kernel<128, 4>, grid, dim3(64 * 4), 0, s, e0, e1a, p);
       else launch_k(attention_mfma_kernel<128, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
-      if (split) launch_k(attn_merge_kernel<bf16_t, 128>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
+      if (split) launch_k(attn_merge_kernel<f16_t, 128>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
     } else {
       return hipErrorInvalidValue;
     }

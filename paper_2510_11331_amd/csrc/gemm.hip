@@ -22,8 +22,8 @@
 //     barriers; it has no branches either (padding rows and groups past a
 //     wave's share are out-of-range buffer loads that return zero), so
 //     vmcnt only ever waits for the older step group;
-//   * bf16: one v_mfma_f32_16x16x32_bf16 per 16-byte unit; fp32: four
-//     v_mfma_f32_16x16x4_f32;
+//   * bf16 models (operands in fp16, see f16_t): one v_mfma_f32_16x16x32_f16
+//     per 16-byte unit; fp32: four v_mfma_f32_16x16x4_f32;
 //   * the KW partial tiles are added in wave order through LDS in one round
 //     (deterministic); K is never split across workgroups (a cross-workgroup
 //     reduction needs a device-scope release per workgroup, which costs more
@@ -41,18 +41,19 @@
 #include "sd_internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace sd {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 template <typename T> struct Mfma;
-template <> struct Mfma<bf16_t> {
+template <> struct Mfma<f16_t> {
   __device__ __forceinline__ static f32x4 step(u32x4 a, u32x4 b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                  0, 0);
   }
 };
 template <> struct Mfma<float> {
@@ -452,7 +453,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 // rows, so the operands are staged once per workgroup in LDS and shared.
 // A workgroup of 4 waves (2 x 2) owns a BM x BN = 32 MF x 32 NF output tile;
 // wave (wm, wn) owns the 16 MF x 16 NF sub-tile at (wm 16 MF, wn 16 NF).
-// K advances in stages of two k-steps (64 bf16); a stage is the
+// K advances in stages of two k-steps (64 fp16); a stage is the
 // 2 (BM + BN) / 16 1 KB fragments, which the 4 waves load straight into
 // one of NB LDS buffers (buffer loads with an LDS destination: lane i's
 // 16 bytes land at the buffer's fragment base + 16 i, no registers held).
@@ -470,7 +471,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 // weights are fetched from HBM once and re-read from that XCD's L2.
 template <int MF, int NF, int EPI, int NB>
 __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
-  using T = bf16_t;
+  using T = f16_t;
   constexpr int BM = 32 * MF, BN = 32 * NF;
   constexpr int FA = 2 * BM / 16, FW = 2 * BN / 16, FS = FA + FW;   // fragments per stage
   static_assert(NB >= 2 && (NB - 2) * (MF + NF) < 64, "stages in flight");
@@ -741,9 +742,12 @@ hipError_t launch_gemm_rows(int epi, int mf, int nf, const GemmParams& p, hipStr
   }
 }
 
-// row-major [N, K] -> MFMA-tile layout, one 16-byte unit per thread
-template <typename T>
-__global__ void pack_linear_kernel(const T* src, T* dst, int N, int K) {
+// row-major [N, K] -> MFMA-tile layout, one 16-byte unit per thread; bf16
+// sources (S = bf16_t) are converted to fp16 (T = f16_t) on the way: exact
+// from 2^-14 up, smaller magnitudes round to the fp16 subnormal grid
+template <typename S, typename T>
+__global__ void pack_linear_kernel(const S* src, T* dst, int N, int K) {
+  static_assert(sizeof(S) == sizeof(T), "same element size");
   constexpr int EPL = Tile<T>::EPL, EPK = Tile<T>::EPK;
   const int ks = K / EPK;
   const size_t units = (size_t)N * K / EPL;
@@ -753,7 +757,15 @@ __global__ void pack_linear_kernel(const T* src, T* dst, int N, int K) {
     const int s = (int)(ts % ks), t = (int)(ts / ks);
     const int r = 16 * t + (lane & 15);
     const int k = s * EPK + (lane >> 4) * EPL;
-    *(uint4*)(dst + u * EPL) = *(const uint4*)(src + (size_t)r * K + k);
+    uint4 v = *(const uint4*)(src + (size_t)r * K + k);
+    if constexpr (!std::is_same_v<S, T>) {
+      uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        w[i] = (uint32_t)f2h(bf2f((bf16_t)(w[i] & 0xffffu))) | ((uint32_t)f2h(bf2f((bf16_t)(w[i] >> 16))) << 16);
+      v = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    *(uint4*)(dst + u * EPL) = v;
   }
 }
 
@@ -763,9 +775,11 @@ hipError_t launch_pack_linear(int dtype, const void* src, void* dst, int N, int 
   const size_t units = (size_t)N * K * esz / 16;
   const int blocks = (int)std::min<size_t>((units + 255) / 256, 65536);
   if (dtype == 0)
-    hipLaunchKernelGGL(pack_linear_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, (const bf16_t*)src, (bf16_t*)dst, N, K);
+    hipLaunchKernelGGL((pack_linear_kernel<bf16_t, f16_t>), dim3(blocks), dim3(256), 0, s, (const bf16_t*)src,
+                       (f16_t*)dst, N, K);
   else
-    hipLaunchKernelGGL(pack_linear_kernel<float>, dim3(blocks), dim3(256), 0, s, (const float*)src, (float*)dst, N, K);
+    hipLaunchKernelGGL((pack_linear_kernel<float, float>), dim3(blocks), dim3(256), 0, s, (const float*)src,
+                       (float*)dst, N, K);
   return hipGetLastError();
 }
 
@@ -825,7 +839,7 @@ bool gemm_config_ok(int dtype, int epi, int nt, int mt, int kw, int grid_x, int 
                     const GemmParams& p) {
   const size_t kbytes = (size_t)p.K * (dtype == 0 ? 2 : 4);
   if (mt < 1 || mt > 4 || kw < 1 || kw > 4) return false;
-  // instantiated tiles: 48 columns for QKV only, 96 columns (bf16 SwiGLU,
+  // instantiated tiles: 48 columns for QKV only, 96 columns (16-bit SwiGLU,
   // 3 row tiles) for balanced mode only
   switch (nt) {
     case 1: if (epi == EPI_SWIGLU) return false; break;
@@ -865,11 +879,11 @@ hipError_t launch_gemm(int dtype, int epi, int nt, int mt, int kw, int grid_x, i
   }
   const int threads = 64 * kw;
   if (dtype == 0) {
-    if (epi == EPI_STORE) return launch_nt<bf16_t, EPI_STORE>(nt, mt, grid, threads, q, s, e0, e1);
-    if (epi == EPI_RESID) return launch_nt<bf16_t, EPI_RESID>(nt, mt, grid, threads, q, s, e0, e1);
-    if (epi == EPI_QKV) return launch_nt<bf16_t, EPI_QKV>(nt, mt, grid, threads, q, s, e0, e1);
-    if (epi == EPI_PART) return launch_nt<bf16_t, EPI_PART>(nt, mt, grid, threads, q, s, e0, e1);
-    return launch_nt<bf16_t, EPI_SWIGLU>(nt, mt, grid, threads, q, s, e0, e1);
+    if (epi == EPI_STORE) return launch_nt<f16_t, EPI_STORE>(nt, mt, grid, threads, q, s, e0, e1);
+    if (epi == EPI_RESID) return launch_nt<f16_t, EPI_RESID>(nt, mt, grid, threads, q, s, e0, e1);
+    if (epi == EPI_QKV) return launch_nt<f16_t, EPI_QKV>(nt, mt, grid, threads, q, s, e0, e1);
+    if (epi == EPI_PART) return launch_nt<f16_t, EPI_PART>(nt, mt, grid, threads, q, s, e0, e1);
+    return launch_nt<f16_t, EPI_SWIGLU>(nt, mt, grid, threads, q, s, e0, e1);
   }
   if (epi == EPI_STORE) return launch_nt<float, EPI_STORE>(nt, mt, grid, threads, q, s, e0, e1);
   if (epi == EPI_RESID) return launch_nt<float, EPI_RESID>(nt, mt, grid, threads, q, s, e0, e1);

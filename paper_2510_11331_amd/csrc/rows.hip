@@ -39,15 +39,23 @@ template <> struct Vec4<bf16_t> {
                                     (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
   }
 };
+template <> struct Vec4<f16_t> {
+  __device__ __forceinline__ static void store_at(f16_t* p, size_t off, float4 v) {
+    *(uint2*)(p + off) = make_uint2((uint32_t)f2h(v.x) | ((uint32_t)f2h(v.y) << 16),
+                                    (uint32_t)f2h(v.z) | ((uint32_t)f2h(v.w) << 16));
+  }
+};
 template <> struct Vec4<float> {
   __device__ __forceinline__ static float4 load(const float* p, int i4) { return ((const float4*)p)[i4]; }
   __device__ __forceinline__ static void store_at(float* p, size_t off, float4 v) { *(float4*)(p + off) = v; }
 };
 
 // row r of out (MFMA-tile layout) = x / sqrt(mean(x^2) + eps) * gain for a
-// register-resident row x (float4 i of the row is v[k], i = threadIdx.x + 256 k)
-template <typename T>
-__device__ void norm_store(const float4 (&v)[RV], int d, const T* gain, T* out, int r, float eps, float* red) {
+// register-resident row x (float4 i of the row is v[k], i = threadIdx.x + 256 k);
+// TW: storage type of the gains (the model's weights), TA: of the output
+// (the matrix-product operands: fp16 for a bf16 model)
+template <typename TW, typename TA>
+__device__ void norm_store(const float4 (&v)[RV], int d, const TW* gain, TA* out, int r, float eps, float* red) {
   const int d4 = d >> 2;
   float ss = 0.f;
 #pragma unroll
@@ -59,14 +67,14 @@ __device__ void norm_store(const float4 (&v)[RV], int d, const T* gain, T* out, 
   for (int k = 0; k < RV; ++k) {
     const int i = threadIdx.x + 256 * k;
     if (i < d4) {
-      const float4 g = Vec4<T>::load(gain, i);
-      Vec4<T>::store_at(out, Tile<T>::off(r, 4 * i, d),
+      const float4 g = Vec4<TW>::load(gain, i);
+      Vec4<TA>::store_at(out, Tile<TA>::off(r, 4 * i, d),
                         make_float4(v[k].x * inv * g.x, v[k].y * inv * g.y, v[k].z * inv * g.z, v[k].w * inv * g.w));
     }
   }
 }
 
-template <typename T>
+template <typename T, typename TA>
 __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
   __shared__ float red[4];
   const int r = blockIdx.x;
@@ -91,7 +99,7 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
       }
       for (int i = threadIdx.x; i < p.d; i += 256) {
         p.x[(size_t)r * p.d + i] = 0.f;
-        Store<T>::store((T*)p.xn, Tile<T>::off(r, i, p.d), 0.f);
+        Store<TA>::store((TA*)p.xn, Tile<TA>::off(r, i, p.d), 0.f);
       }
       return;
     }
@@ -147,12 +155,12 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
     const int i = threadIdx.x + 256 * k;
     if (i < d4) x[i] = v[k];
   }
-  norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn, r, p.eps, red);
+  norm_store<T, TA>(v, p.d, (const T*)p.gain, (TA*)p.xn, r, p.eps, red);
 }
 
 // NS: number of K-split partial sums to add into the residual row first (all
 // loads are issued before the first add; the adds follow split order)
-template <typename T, int NS>
+template <typename T, typename TA, int NS>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(NormParams p) {
   __shared__ float red[4];
   const int r = blockIdx.x;
@@ -184,21 +192,21 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormParams p) {
       if (i < d4) x[i] = v[k];
     }
   }
-  norm_store<T>(v, p.d, (const T*)p.gain, (T*)p.xn, r, p.eps, red);
+  norm_store<T, TA>(v, p.d, (const T*)p.gain, (TA*)p.xn, r, p.eps, red);
 }
 
 hipError_t launch_rows_embed(int dtype, const RowsParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
   if ((p.d & 3) || p.d > 256 * 4 * RV) return hipErrorInvalidValue;
-  if (dtype == 0) hipLaunchKernelGGL(rows_embed_kernel<bf16_t>, dim3(p.M), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL(rows_embed_kernel<float>, dim3(p.M), dim3(256), 0, s, p);
+  if (dtype == 0) hipLaunchKernelGGL((rows_embed_kernel<bf16_t, f16_t>), dim3(p.M), dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((rows_embed_kernel<float, float>), dim3(p.M), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
 template <int NS>
 static hipError_t launch_norm_ns(int dtype, const NormParams& p, hipStream_t s) {
-  if (dtype == 0) hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, NS>), dim3(p.M), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((rmsnorm_kernel<float, NS>), dim3(p.M), dim3(256), 0, s, p);
+  if (dtype == 0) hipLaunchKernelGGL((rmsnorm_kernel<bf16_t, f16_t, NS>), dim3(p.M), dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((rmsnorm_kernel<float, float, NS>), dim3(p.M), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

@@ -1,6 +1,6 @@
 // Serving scheduler: the paper's runtime / pipeline latency model, the
-// batching dynamic program and the speculation-length search (Sections III
-// and IV; see include/sd_sched.h for the model).  Host code only.
+// batching dynamic program and the speculation-length search (Sections II-C,
+// II-D and III; see include/sd_sched.h for the model).  Host code only.
 #include "sd.h"
 #include "sd_sched.h"
 

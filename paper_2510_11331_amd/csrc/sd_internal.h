@@ -12,6 +12,13 @@ namespace sd {
 // ---------------------------------------------------------------- numerics
 
 typedef uint16_t bf16_t;  // raw bf16 bit pattern in memory
+// IEEE binary16.  A bf16 model is computed with fp16 operands: its packed
+// weight matrices are converted to fp16 once (sd_pack_linear; exact for
+// every bf16 value of magnitude >= 2^-14, smaller ones round to fp16's
+// subnormal grid of 2^-24), and its matrix-product inputs and KV cache are
+// rounded to fp16 (11 significant bits against bf16's 8), at the same memory
+// cost and matrix-instruction rate.  Embedding rows and norm gains stay bf16.
+typedef _Float16 f16_t;
 
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
@@ -21,6 +28,10 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
   u += 0x7FFFu + ((u >> 16) & 1u);
   return (bf16_t)(u >> 16);
 }
+
+// fp16 bit pattern of f, rounded to nearest even (v_cvt_f16_f32)
+__device__ __forceinline__ uint16_t f2h(float f) { return __builtin_bit_cast(uint16_t, (f16_t)f); }
+__device__ __forceinline__ float h2f(uint16_t h) { return (float)__builtin_bit_cast(f16_t, h); }
 
 // MFMA-tile layout of a matrix-product operand X[R, K] (weights R = N,
 // activations R = M rows padded to 16): a k-step is 64 bytes of a row
@@ -76,6 +87,10 @@ template <typename T> struct Store;
 template <> struct Store<bf16_t> {
   __device__ __forceinline__ static float load(const bf16_t* p, size_t i) { return bf2f(p[i]); }
   __device__ __forceinline__ static void store(bf16_t* p, size_t i, float v) { p[i] = f2bf(v); }
+};
+template <> struct Store<f16_t> {
+  __device__ __forceinline__ static float load(const f16_t* p, size_t i) { return (float)p[i]; }
+  __device__ __forceinline__ static void store(f16_t* p, size_t i, float v) { p[i] = (f16_t)v; }
 };
 template <> struct Store<float> {
   __device__ __forceinline__ static float load(const float* p, size_t i) { return p[i]; }

@@ -84,3 +84,52 @@ def compare_greedy(gpu_tokens: List[int], ref_tokens: List[int], ref_logits: np.
             raise AssertionError(f"greedy token {i}: gpu {gpu_tokens[i]} oracle {ref_tokens[i]} "
                                  f"(oracle top-2 gap {gap:.3g})")
     return n, None
+
+
+def greedy_stream_report(target, prompts, emitted, acc, logits, n_new, bound, tie=1e-3):
+    """Greedy stream of a GPU run against the oracle target, teacher-forced
+    on the GPU's own emitted prefix (so the comparison resynchronises after
+    any divergence).  emitted: per task the GPU's tokens; acc [steps, B] and
+    logits [steps, B, gamma+1, V] of the run: rows 0..a of a step are the
+    logits that chose its emitted tokens.  Asserts, at every position of the
+    first n_new tokens of every task: the GPU token is the arg-max of the
+    GPU row (lowest index on ties); the row is within `bound` of the plain
+    and of the rounded oracle's (per-row max abs error over max abs); where
+    the token is not the plain oracle's arg-max, the oracle's top-2 gap is
+    a near tie (< tie) or is covered by the two tokens' logit errors.
+    Returns the counts and the gaps of the divergences."""
+    B = len(prompts)
+    rows = [[] for _ in range(B)]                 # GPU logits of each emitted position
+    for n in range(acc.shape[0]):
+        for k in range(B):
+            for j in range(int(acc[n, k]) + 1):
+                if len(rows[k]) < n_new:
+                    rows[k].append(logits[n, k, j])
+    toks = [list(emitted[k][:n_new]) for k in range(B)]
+    assert all(len(r) == n_new and len(t) == n_new for r, t in zip(rows, toks))
+    seqs = [list(prompts[k]) + toks[k][:-1] for k in range(B)]
+    ref = {"plain": target.unrounded().sequence_logits(seqs, n_new), "rounded": target.sequence_logits(seqs, n_new)}
+    worst = {f: 0.0 for f in ref}
+    near, div, div_gaps = 0, 0, []
+    for k in range(B):
+        for i in range(n_new):
+            z = np.asarray(rows[k][i], dtype=np.float64)
+            assert toks[k][i] == osp.argmax_lowest(z), (k, i)
+            for f, zz in ref.items():
+                worst[f] = max(worst[f], float(np.abs(z - zz[k][i]).max() / np.abs(zz[k][i]).max()))
+            zr = ref["plain"][k][i]
+            o = osp.argmax_lowest(zr)
+            if o == toks[k][i]:
+                continue
+            gap = top2_gap(zr)
+            if gap < tie:
+                near += 1
+                continue
+            dz = np.abs(z - zr)
+            assert gap <= dz[o] + dz[toks[k][i]] + 1e-9, (k, i, gap, dz[o], dz[toks[k][i]])
+            div += 1
+            div_gaps.append(round(gap, 4))
+    for f, e in worst.items():
+        assert e < bound, (f, e)
+    return {"positions": B * n_new, "near_ties": near, "divergences": div, "divergence_gaps": sorted(div_gaps),
+            "worst_rel_logit_err": worst}

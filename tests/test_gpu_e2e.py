@@ -121,6 +121,17 @@ def test_two_streams_equal_one_stream():
         eng.close()
     for (a0, o0), (a1, o1) in zip(res[0], res[1]):
         assert np.array_equal(a0, a1) and np.array_equal(o0, o1)
+    # and both are the oracle's stream for every task (task k of batch m is
+    # slot 2 m + j, with the uniforms of task id 2 m + j)
+    tgt, dft = om.Model(t, tw), om.Model(d, dw)
+    for m, (acc, out) in enumerate(res[1]):
+        for j in range(2):
+            k = 2 * m + j
+            ut = synth.uniform_table(3, [k], n_steps, gamma)[:, 0]
+            task = osd.SDTask(tgt, dft, prompts[k])
+            for n in range(n_steps):
+                a, em = task.step(gamma, ut[n], 0.2)
+                assert acc[n, j] == a and list(out[n, j, :a + 1]) == em, (k, n)
 
 
 def test_small_bf16_gqa_logits_and_greedy():

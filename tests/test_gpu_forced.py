@@ -67,6 +67,51 @@ def _forced_run(tshape, dshape, B, gamma, prompt_len, n_forced, alpha):
     return acc, extra
 
 
+@pytest.mark.parametrize("alpha", [0.5, 0.8])
+def test_tiny_forced_run_equals_the_oracle(alpha):
+    """The forced rule on the tiny pair, decision by decision: both sides get
+    the oracle's greedy continuation of the target as the reference, the
+    same uniforms and alpha; the GPU's accepted lengths and emitted tokens
+    are the oracle's SD run with the same forcing (sd_generate(force=...))."""
+    import torch
+    from paper_2510_11331_amd import emitted_tokens
+    from paper_2510_11331_amd.engine import uniforms_device
+    from oracle import model as om, sd as osd
+    say("tiny forced against the oracle", alpha)
+    w = synth.WORKLOADS["tiny"]
+    t, d, gamma, B, n_steps = w.target, w.draft, 4, 4, 12
+    tw, dw = synth.model_weights(t, 1), synth.model_weights(d, 2)
+    prompts = synth.prompts(B, w.prompt_len, t.vocab)
+    tgt, dft = om.Model(t, tw), om.Model(d, dw)
+    n_cont = n_steps * (gamma + 1) + 2
+    cont = np.array([list(prompts[k]) + osd.ar_generate(tgt, prompts[k], n_cont, greedy=True) for k in range(B)],
+                    dtype=np.int32)
+    eng = make_engine(t, d, tw, dw, max_slots=B, max_batch=B, gamma_max=gamma,
+                      max_ctx=w.prompt_len + (n_steps + 1) * (gamma + 1) + 16, greedy=True)
+    slots = list(range(B))
+    eng.prefill(slots, prompts, [(n_steps + 1) * (gamma + 1)] * B)
+    b = eng.batch(slots, gamma)
+    b.set_force(cont, alpha)
+    ut = synth.uniform_table(42, slots, n_steps, gamma)
+    u = uniforms_device(ut)
+    accs, outs = [], []
+    for n in range(n_steps):
+        eng.step(b, u[n])
+        accs.append(b.n_acc.clone())
+        outs.append(b.out_tok.clone())
+    torch.cuda.synchronize()
+    acc = torch.stack(accs).cpu().numpy()
+    out = torch.stack(outs).cpu().numpy()
+    assert eng.check_flags() == 0
+    eng.close()
+    bound = osd.force_threshold(alpha)
+    for k in range(B):
+        task = osd.SDTask(tgt, dft, prompts[k])
+        for n in range(n_steps):
+            a, em = task.step(gamma, ut[n, k], greedy=True, force=(cont[k], bound))
+            assert acc[n, k] == a and list(out[n, k, :a + 1]) == em, (k, n, acc[n, k], a)
+
+
 @pytest.mark.parametrize("alpha", [0.5, 0.8, 1.0])
 def test_tiny_forced_emits_greedy_sequence_and_follows_eq_ol(alpha):
     say("tiny forced", alpha)

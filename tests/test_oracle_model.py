@@ -57,8 +57,12 @@ def test_weights_decode_roundtrip():
     shape = tiny_shape("bf16")
     w = synth.model_weights(shape, seed=3, names=["l0.wq"])
     f = om.weights_to_f64(w, "bf16")["l0.wq"]
-    t = torch.from_numpy(w["l0.wq"].view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    # a bf16 pattern is the upper half of the float32 with the same value
+    t = (w["l0.wq"].astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
     assert np.array_equal(f, t)
+    # and hand values: 0x3F80 = 1.0, 0xC040 = -3.0, 0x0001 = 2^-133 (smallest subnormal)
+    hand = om.weights_to_f64({"x": np.array([0x3F80, 0xC040, 0x0001, 0x7F7F], np.uint16)}, "bf16")["x"]
+    assert list(hand[:3]) == [1.0, -3.0, 2.0 ** -133] and hand[3] == float.fromhex("0x1.fep127")
 
 # ---------------------------------------------------------------- building blocks
 
@@ -166,15 +170,56 @@ def test_decode_rows_vs_torch_full_forward_bf16():
     toks = list(np.random.default_rng(7).integers(0, shape.vocab, 11))
     c = m.new_cache()
     got = np.stack([m.decode_row(c, t, i) for i, t in enumerate(toks)])
-    rnd = lambda t: torch.from_numpy(om.round_bf16(t.numpy()))
-    want = torch_reference_logits(shape, m.w, toks, rnd)
-    # a bf16 storage point can flip by one ulp when float64 rounding order
+    # fp16 operands at every storage point and for the matrices (round_fp16
+    # is pinned on its own below; torch's float64 -> float16 conversion goes
+    # through float32, two roundings, so it is not used here)
+    rnd = lambda t: torch.from_numpy(om.round_fp16(t.numpy()))
+    ops = {k: (om.round_fp16(v) if om.is_matrix(k) else v) for k, v in m.w.items()}
+    want = torch_reference_logits(shape, ops, toks, rnd)
+    # a storage point can flip by one ulp when float64 rounding order
     # differs; the two must otherwise agree
     rel = np.abs(got - want).max() / np.abs(want).max()
     assert rel < 1e-6, rel
     # and the rounding points matter: without them the logits move visibly
     plain = torch_reference_logits(shape, m.w, toks)
-    assert np.abs(got - plain).max() / np.abs(plain).max() > 1e-4
+    assert np.abs(got - plain).max() / np.abs(plain).max() > 1e-5
+
+
+def test_round_fp16_hand_cases_and_library():
+    one, ulp = 1.0, 2.0 ** -10                # fp16 spacing in [1, 2)
+    cases = [(one + ulp / 2, one), (one + 1.5 * ulp, one + 2 * ulp),            # ties to even
+             (one + ulp / 2 + 2.0 ** -40, one + ulp),                           # one rounding, not two
+             (-(one + 1.5 * ulp), -(one + 2 * ulp)), (65504.0, 65504.0),
+             (2.0 ** -24, 2.0 ** -24), (2.0 ** -25, 0.0), (3 * 2.0 ** -25, 2.0 ** -23),   # subnormals
+             (3e-5, round(3e-5 / 2.0 ** -24) * 2.0 ** -24)]
+    for x, want in cases:
+        assert float(om.round_fp16(x)) == want, (x, float(om.round_fp16(x)), want)
+    x = np.random.default_rng(2).standard_normal(100000).astype(np.float32) * 3
+    want = torch.from_numpy(x).to(torch.float16).to(torch.float64).numpy()   # one rounding from float32
+    assert np.array_equal(om.round_fp16(x.astype(np.float64)), want)
+
+
+def test_bf16_model_operands():
+    """The products of a bf16 model read each matrix as fp16: the bf16 value
+    itself from 2^-14 up, the fp16 subnormal grid below; embedding rows and
+    norm gains are read as they are; the plain form reads nothing rounded."""
+    shape = tiny_shape("bf16", 2)
+    w = synth.model_weights(shape, seed=18)
+    m = om.Model(shape, w)
+    for k, v in m.w.items():
+        if om.is_matrix(k):
+            big = np.abs(v) >= 2.0 ** -14
+            assert np.array_equal(m.ops[k][big], v[big]), k
+            assert np.all(np.abs(m.ops[k] - v) <= 2.0 ** -25), k
+            assert np.array_equal(m.ops[k], om.round_fp16(v))
+        else:
+            assert m.ops[k] is v, k
+    assert {k for k in m.w if om.is_matrix(k)} == {k for k in m.w if k == "lm_head" or k.split(".")[-1] in (
+        "wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")}
+    assert m.unrounded().ops is m.w
+    lazy = om.Model(shape, w, lazy=True)
+    for k in m.w:
+        assert np.array_equal(lazy.ops[k], m.ops[k]), k
 
 
 def test_kv_incremental_equals_batched_rows():
