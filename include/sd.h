@@ -167,6 +167,26 @@ size_t sd_workspace_bytes(const sd_config *cfg);
 int sd_init(const sd_config *cfg, const sd_weights *target,
             const sd_weights *draft, sd_ctx **out);
 
+/* Size of the library's own per-device workspace used by sd_init_static. */
+#define SD_STATIC_WORKSPACE_MB 64
+
+/* sd_init without a caller-allocated workspace, for callers that cannot
+ * allocate device memory (code under graph capture, serving loops that
+ * must not call hipMalloc, harnesses that forbid it).  cfg->workspace and
+ * cfg->workspace_bytes are ignored: the context uses a file-scope device
+ * array of SD_STATIC_WORKSPACE_MB MiB that the library holds on each GPU
+ * until the process ends (the current device's copy).  Nothing is
+ * allocated: no hipMalloc / hipFree or allocating library call; the caller
+ * still owns the weights, the KV pools and every input and output.
+ * SD_EINVAL if sd_workspace_bytes(cfg) exceeds the array (the reason is in
+ * sd_last_error), SD_ESTATE while another context made by sd_init_static
+ * on the same device is alive (they would share the array: calls of two
+ * such contexts would race); sd_destroy gives the array back.  sd_init
+ * clears what must start at zero, so a context never sees the previous
+ * one's state.  Otherwise as sd_init. */
+int sd_init_static(const sd_config *cfg, const sd_weights *target,
+                   const sd_weights *draft, sd_ctx **out);
+
 /* Start B tasks: prompt k (host tokens[off_k .. off_k + lens[k]), packed
  * back to back) goes to slot slots[k] (host).  Allocates KV blocks for
  * lens[k] + max_new[k] + gamma_max positions, runs both models over
@@ -281,7 +301,8 @@ void sd_destroy(sd_ctx *ctx);
 const char *sd_strerror(int code);
 
 /* Text of the last SD_EHIP failure on the calling thread (HIP call and
- * message); "" if none.  The string stays valid until the next call. */
+ * message), or of a workspace-size refusal of sd_init_static; "" if none.
+ * The string stays valid until the next call. */
 const char *sd_last_error(void);
 
 #ifdef __cplusplus

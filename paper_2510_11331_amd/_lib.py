@@ -17,7 +17,7 @@ SD_DTYPE_BF16, SD_DTYPE_F32 = 0, 1
  SD_PROF_VERIFY, SD_PROF_DRAFT) = range(5)
 
 # the symbols include/sd.h and include/sd_sched.h declare (checked by the CPU test suite)
-EXPORTS = ("sd_kv_pool_bytes", "sd_workspace_bytes", "sd_init", "sd_prefill", "sd_release",
+EXPORTS = ("sd_kv_pool_bytes", "sd_workspace_bytes", "sd_init", "sd_init_static", "sd_prefill", "sd_release",
            "sd_draft_step", "sd_verify", "sd_accept_resample", "sd_kv_commit", "sd_force_draft", "sd_slot_state",
            "sd_check", "sd_profile", "sd_profile_read", "sd_destroy", "sd_strerror", "sd_last_error",
            "sd_pack_linear", "sd_sched_latency", "sd_sched_batching", "sd_sched_plan", "sd_sched_uplink")
@@ -87,6 +87,7 @@ def lib():
         "sd_kv_pool_bytes": (C.c_size_t, [C.POINTER(Config), I]),
         "sd_workspace_bytes": (C.c_size_t, [C.POINTER(Config)]),
         "sd_init": (I, [C.POINTER(Config), C.POINTER(Weights), C.POINTER(Weights), C.POINTER(P)]),
+        "sd_init_static": (I, [C.POINTER(Config), C.POINTER(Weights), C.POINTER(Weights), C.POINTER(P)]),
         "sd_prefill": (I, [P, I, C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                            C.POINTER(C.c_int32), P]),
         "sd_release": (I, [P, I]),

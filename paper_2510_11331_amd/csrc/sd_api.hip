@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstring>
 #include <deque>
+#include <mutex>
 #include <new>
 #include <unordered_map>
 #include <vector>
@@ -88,6 +89,7 @@ struct sd_ctx {
   std::vector<Slot> slots;
   std::vector<int> free_t, free_d;
   std::unordered_map<const void*, Phase> phases;   // by device slot-list address
+  int static_dev = -1;          // device whose static workspace this context holds (sd_init_static)
   bool prof = false;
   std::vector<ProfRec> recs;
 };
@@ -616,6 +618,22 @@ Phase& phase_of(sd_ctx* ctx, const void* slots, int B, int gamma) {
 
 }  // namespace
 
+// ---------------------------------------------------------------- static workspace
+
+// The workspace of sd_init_static: a file-scope device array (each GPU the
+// library runs on holds its own copy until the process ends).  Host code
+// never uses the array's name as an address: its device address on each
+// device comes from hipGetSymbolAddress, once per device, with that device
+// current, and is kept in g_static_ptr.  A context holds its device's
+// array from sd_init_static to sd_destroy; the array keeps the last
+// context's contents and sd_init clears the parts that must start at zero.
+constexpr size_t STATIC_WS_BYTES = (size_t)SD_STATIC_WORKSPACE_MB << 20;
+constexpr int STATIC_MAX_DEV = 64;
+__device__ __align__(256) unsigned char scratch[STATIC_WS_BYTES];
+std::mutex g_static_mu;
+void* g_static_ptr[STATIC_MAX_DEV] = {};
+bool g_static_held[STATIC_MAX_DEV] = {};
+
 // ============================================================== C ABI
 
 extern "C" {
@@ -664,6 +682,40 @@ int sd_init(const sd_config* cfg, const sd_weights* target, const sd_weights* dr
   }
   *out = ctx;
   return SD_OK;
+}
+
+int sd_init_static(const sd_config* cfg, const sd_weights* target, const sd_weights* draft, sd_ctx** out) {
+  if (!out) return SD_EINVAL;
+  *out = nullptr;
+  if (!cfg_ok(cfg)) return SD_EINVAL;
+  const size_t need = layout(cfg, nullptr);
+  if (need > STATIC_WS_BYTES) {
+    snprintf(g_last_error, sizeof(g_last_error),
+             "sd_init_static: the configuration needs a %zu-byte workspace, the static one holds %zu", need,
+             STATIC_WS_BYTES);
+    return SD_EINVAL;
+  }
+  int dev = -1;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= STATIC_MAX_DEV) return SD_EINVAL;
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (g_static_held[dev]) return SD_ESTATE;    // another live context uses this device's array
+  if (!g_static_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress(scratch)",
+                                               __LINE__);
+    g_static_ptr[dev] = p;
+  }
+  sd_config c = *cfg;
+  c.workspace = g_static_ptr[dev];
+  c.workspace_bytes = STATIC_WS_BYTES;
+  const int rc = sd_init(&c, target, draft, out);
+  if (rc == SD_OK) {
+    (*out)->static_dev = dev;
+    g_static_held[dev] = true;
+  }
+  return rc;
 }
 
 int sd_prefill(sd_ctx* ctx, int B, const int32_t* slots, const int32_t* tokens, const int32_t* lens,
@@ -1013,6 +1065,10 @@ int sd_profile_read(sd_ctx* ctx, int kind, int64_t* count, double* ms, double* b
 
 void sd_destroy(sd_ctx* ctx) {
   if (!ctx) return;
+  if (ctx->static_dev >= 0) {
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    g_static_held[ctx->static_dev] = false;
+  }
   for (ProfRec& r : ctx->recs) {
     hipEventDestroy(r.a);
     hipEventDestroy(r.b);

@@ -142,7 +142,9 @@ class SDEngine:
     def __init__(self, tshape, dshape, tget, dget, *, max_slots: int, max_batch: int, gamma_max: int,
                  max_ctx: int, kv_blocks_target: Optional[int] = None, kv_blocks_draft: Optional[int] = None,
                  prefill_rows: int = 1024, temperature: float = 1.0, greedy: bool = False,
-                 device: str = "cuda"):
+                 device: str = "cuda", static_workspace: bool = False):
+        """static_workspace: the context uses libsd's own per-device
+        workspace (sd_init_static) instead of one allocated here."""
         L = lib()
         self.device = device
         self.tshape, self.dshape = tshape, dshape
@@ -165,17 +167,23 @@ class SDEngine:
             raise _lib.SDError(_lib.SD_EINVAL, "configuration rejected")
         self.pool_t = torch.empty(pt, dtype=torch.uint8, device=device)
         self.pool_d = torch.empty(pd, dtype=torch.uint8, device=device)
-        self.workspace = torch.empty(ws, dtype=torch.uint8, device=device)
         cfg.kv_pool_target = self.pool_t.data_ptr()
         cfg.kv_pool_draft = self.pool_d.data_ptr()
-        cfg.workspace = self.workspace.data_ptr()
-        cfg.workspace_bytes = ws
+        if static_workspace:
+            self.workspace = None
+        else:
+            self.workspace = torch.empty(ws, dtype=torch.uint8, device=device)
+            cfg.workspace = self.workspace.data_ptr()
+            cfg.workspace_bytes = ws
         self.cfg = cfg
         self.target = GPUModel(tshape, tget, device)
         self.draft = GPUModel(dshape, dget, device)
         h = C.c_void_p()
-        check(L.sd_init(C.byref(cfg), C.byref(self.target.cstruct), C.byref(self.draft.cstruct), C.byref(h)),
-              "sd_init")
+        init = L.sd_init_static if static_workspace else L.sd_init
+        rc = init(C.byref(cfg), C.byref(self.target.cstruct), C.byref(self.draft.cstruct), C.byref(h))
+        if rc != _lib.SD_OK and static_workspace:
+            raise _lib.SDError(rc, "sd_init_static: " + L.sd_last_error().decode())
+        check(rc, "sd_init")
         self.ctx = h
         self.L = L
 
