@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--workload", default="7b_b8", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch size")
     ap.add_argument("--gamma", type=int, default=0, help="override the workload's gamma")
+    ap.add_argument("--alpha", type=float, default=None,
+                    help="override the forced acceptance rate of a forced-acceptance workload (13B)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="short eager run for rocprofv3 --pmc: a 1 GiB copy kernel (counter calibration) "
@@ -106,7 +108,7 @@ def summarise_counters(fetch_csv: str, write_csv: str) -> None:
             for row in csv.DictReader(f):
                 if row.get("Counter_Name") != counter:
                     continue
-                name = row["Kernel_Name"]
+                name = short_kernel_name(row["Kernel_Name"])
                 key = "copy" if COPY_NAME in name else "gateup" if GATEUP_NAME in name else None
                 if key:
                     vals.setdefault(key, []).append(float(row["Counter_Value"]))
@@ -200,9 +202,39 @@ def cpu_baseline(wl, B, gamma, emitted_per_step, budget_s=10.0, max_tasks=None):
             "step_seconds": round(t_step, 4)}
 
 
+def _unmangle_sd(n: str) -> str:
+    """Readable form of a mangled libsd kernel name that the profiler left
+    mangled (it does not know fp16 template arguments): _ZN2sd<len><name>I
+    <args>E...  with args _Float16 (DF16_), float (f), unsigned short (t),
+    ints (Li<n>E)."""
+    import re
+    m = re.match(r"_ZN2sd(\d+)", n)
+    if not m:
+        return n
+    k = int(m.group(1))
+    name = n[m.end():m.end() + k]
+    rest = n[m.end() + k:]
+    if not rest.startswith("I"):
+        return "sd::" + name
+    args, i = [], 1
+    while i < len(rest) and rest[i] != "E":
+        if rest.startswith("DF16_", i):
+            args.append("_Float16"); i += 5
+        elif rest[i] in "ft":
+            args.append("float" if rest[i] == "f" else "unsigned short"); i += 1
+        else:
+            mm = re.match(r"Li(\d+)E", rest[i:])
+            if not mm:
+                return n
+            args.append(mm.group(1)); i += mm.end()
+    return f"sd::{name}<{', '.join(args)}>"
+
+
 def short_kernel_name(n: str) -> str:
     """"void sd::gemm_kernel<...>(sd::GemmParams) [clone .kd]" -> "sd::gemm_kernel<...>"."""
     n = n.split(" [clone")[0].strip()
+    if n.startswith("_Z"):
+        return _unmangle_sd(n)
     if n.startswith("void "):
         n = n[5:]
     if n.endswith(")"):
@@ -219,8 +251,9 @@ def short_kernel_name(n: str) -> str:
 def counters_summary(path: str) -> None:
     """Markdown table of a rocprofv3 --pmc counter_collection.csv: per kernel
     and grid size, the dispatches, the median duration under counter
-    collection, the median of every collected counter, and for MfmaFlopsBF16
-    the achieved dense bf16 rate against MI355X's 2.5 PFLOP/s."""
+    collection, the median of every collected counter, and for the matrix
+    FLOP counters (MfmaFlopsF16 / MfmaFlopsBF16) the achieved dense rate
+    against MI355X's 2.5 PFLOP/s (fp16 and bf16 alike)."""
     import csv
     from collections import defaultdict
     vals, durs, counters = defaultdict(lambda: defaultdict(list)), defaultdict(dict), []
@@ -232,18 +265,19 @@ def counters_summary(path: str) -> None:
                 counters.append(c)
             vals[key][c].append(float(r["Counter_Value"]))
             durs[key][r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    flop = next((c for c in ("MfmaFlopsF16", "MfmaFlopsBF16") if c in counters), None)
     head = "| kernel (grid) | dispatches | median us | " + " | ".join(f"median {c}" for c in counters)
-    if "MfmaFlopsBF16" in counters:
-        head += " | bf16 TFLOP/s | of 2.5 PFLOP/s"
+    if flop:
+        head += " | MFMA TFLOP/s | of 2.5 PFLOP/s"
     print(head + " |")
-    print("|---|---:|---:|" + "---:|" * len(counters) + ("---:|---:|" if "MfmaFlopsBF16" in counters else ""))
+    print("|---|---:|---:|" + "---:|" * len(counters) + ("---:|---:|" if flop else ""))
     for key in sorted(vals, key=lambda k: -sum(durs[k].values())):
         d = list(durs[key].values())
         us = float(np.median(d))
         row = f"| `{key[0]}` ({key[1]}) | {len(d)} | {us:.1f} | " + " | ".join(
             f"{float(np.median(vals[key][c])):.4g}" if vals[key][c] else "" for c in counters)
-        if "MfmaFlopsBF16" in counters:
-            fl = float(np.median(vals[key]["MfmaFlopsBF16"])) if vals[key]["MfmaFlopsBF16"] else 0.0
+        if flop:
+            fl = float(np.median(vals[key][flop])) if vals[key][flop] else 0.0
             tf = fl / (us * 1e-6) / 1e12 if us > 0 else 0.0
             row += f" | {tf:.0f} | {tf / 2500:.3f}"
         print(row + " |")
@@ -599,7 +633,7 @@ def gamma_sweep(args) -> None:
     then the verify pass and the gamma draft calls alone (graph replay, p50)."""
     import torch
     from paper_2510_11331_amd import SDEngine, StepGraph, generate_graph
-    wl = synth.WORKLOADS[args.workload]
+    wl = workload_of(args)
     gammas = [int(x) for x in args.sweep_gamma.split(",")]
     B, K, W = args.batch or wl.batch, args.steps, args.warmup
     t, d = wl.target, wl.draft
@@ -651,6 +685,16 @@ def gamma_sweep(args) -> None:
         for s_ in slots:
             eng.release(s_)
     eng.close()
+
+
+def workload_of(args):
+    """The named workload, with the forced acceptance rate overridden by --alpha."""
+    import dataclasses
+    wl = synth.WORKLOADS[args.workload]
+    if args.alpha is not None:
+        assert wl.alpha_forced is not None, "--alpha applies to a forced-acceptance workload"
+        wl = dataclasses.replace(wl, alpha_forced=float(args.alpha))
+    return wl
 
 
 def copy_ceiling_gbs(nbytes: int = 1 << 30, reps: int = 10) -> float:
@@ -733,7 +777,7 @@ def main():
     from paper_2510_11331_amd import SDEngine, StepGraph, generate, generate_graph, emitted_tokens
     from paper_2510_11331_amd import _lib
 
-    wl = synth.WORKLOADS[args.workload]
+    wl = workload_of(args)
     B = args.batch or wl.batch
     gamma = args.gamma or wl.gamma
     K, W = args.steps, args.warmup
@@ -869,13 +913,15 @@ def main():
     gu_ms = ms_gu / max(n_gu, 1)
     gu_bytes = bytes_gu / max(n_gu, 1)
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
-    # algorithmic bytes of one verify step: every weight once, the cached K/V
-    # of every task once per layer, the new K/V, logits / probabilities; the
-    # verify latency was taken on batch 0 after its W + K steps, so its
-    # context is the prompt plus the tokens those steps committed
+    # algorithmic bytes of one verify step: every weight read once (of the
+    # embedding table only the B (gamma+1) rows the pass looks up), the
+    # cached K/V of every task once per layer, the new K/V, logits /
+    # probabilities; the verify latency was taken on batch 0 after its W + K
+    # steps, so its context is the prompt plus the tokens those steps committed
     P = float(np.mean(lens[:B])) + float((acc + 1).mean()) * (W + K)
     kv_bytes = t.n_layers * 2 * t.n_kv_heads * t.head_dim * 2 * B * P
-    step_bytes = 2 * t.n_params() + kv_bytes + 2 * B * (gamma + 1) * t.vocab * 4
+    weight_bytes = 2 * (t.n_params() - t.vocab * t.d_model) + 2 * B * (gamma + 1) * t.d_model
+    step_bytes = weight_bytes + kv_bytes + 2 * B * (gamma + 1) * t.vocab * 4
     verify_p50 = float(np.median(verify_ms))
     copy_gbs = copy_ceiling_gbs()
 
