@@ -220,6 +220,8 @@ hipError_t launch_rmsnorm(int dtype, const NormParams& p, hipStream_t s) {
     case 2: return launch_norm_ns<2>(dtype, p, s);
     case 3: return launch_norm_ns<3>(dtype, p, s);
     case 4: return launch_norm_ns<4>(dtype, p, s);
+    case 5: return launch_norm_ns<5>(dtype, p, s);
+    case 6: return launch_norm_ns<6>(dtype, p, s);
     default: return hipErrorInvalidValue;
   }
 }

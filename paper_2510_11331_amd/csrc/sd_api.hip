@@ -23,7 +23,8 @@ using namespace sd;
 namespace {
 
 constexpr int KV_BLOCK = 16;
-constexpr int MAX_KSPLIT = 4;   // K splits of a residual projection (partial sums in the workspace)
+constexpr int MAX_KSPLIT = 6;   // K splits of a residual projection (partial sums in the workspace)
+constexpr int SKINNY_MAX_KSPLIT = 4;   // of those on the skinny GEMM
 
 struct ModelRT {
   sd_model_cfg c{};
@@ -352,7 +353,7 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
   } else if (epi == EPI_RESID && split_ok) {
     auto splits = [&](int nt) {
       const int gx = N / (16 * nt);
-      return std::min(std::min(MAX_KSPLIT, std::max(1, (256 + gx - 1) / gx)), std::max(1, groups / 4));
+      return std::min(std::min(SKINNY_MAX_KSPLIT, std::max(1, (256 + gx - 1) / gx)), std::max(1, groups / 4));
     };
     g.nt = 1;
     if (g.mt >= 2 && pick(2) && groups / splits(2) >= 4 * g.kw) g.nt = 2;
@@ -377,18 +378,39 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
 // and 13B B = 64 verify shapes (weights streamed from HBM): 13B gate/up at
 // M = 320 109 us against 205 us on the skinny GEMM, LM head 108 against 245.
 // The residual projections (N = d_model) from 128 to 640 rows run on
-// 128 x 128 row tiles with K split in 4 when the caller can add partial sums
+// 128 x 128 row tiles with K split when the caller can add partial sums
 // (split_ok; *ks receives the split): 7B at M = 160: O 14.6-15.6 us and down
 // 29.8-32.3 us, against about 22 and 64 on the skinny GEMM; 13B at M = 320:
-// O 24.8 us, down 58.3, against 40.8 and 93.2 unsplit.  Without a split they
-// run on 128 x 64 tiles from 256 to 640 rows and on the skinny GEMM below.
-// Returns false where the skinny GEMM runs.
+// O 24.8 us, down 58.3, against 40.8 and 93.2 unsplit.  The split is chosen
+// for the grid (column tiles x row tiles x splits): the largest split up to
+// MAX_KSPLIT that keeps it within 512 workgroups (two per CU), or, when that
+// grid would leave CUs with one workgroup and others with two (257 to 447
+// workgroups), the largest that keeps it within 256 (one per CU), if that
+// still splits.  Measured against the fixed four-way split (weights streamed
+// from HBM): 13B down at M = 192 / 256 / 448 / 512: 44.4 / 53.9 / 77.1 / 88.5
+// us against 58.6 / 70.4 / 107.8 / 125.2 (O: 20.6 / 24.5 / 30.8 / 36.8
+// against 23.9 / 28.3 / 43.2 / 50.7); 7B down at M = 320 / 576: 40.6 / 59.5
+// against 45.4 / 87.6.  Without a split they run on 128 x 64 tiles from 256
+// to 640 rows and on the skinny GEMM below.  Returns false where the skinny
+// GEMM runs.
+int resid_ksplit(int M, int N) {
+  const int tiles = (N / 128) * ((M + 127) / 128);
+  int k512 = 0, k256 = 0;
+  for (int k = 1; k <= MAX_KSPLIT; ++k) {
+    if (tiles * k <= 512) k512 = k;
+    if (tiles * k <= 256) k256 = k;
+  }
+  const int g = tiles * k512;
+  return g > 256 && g < 448 && k256 >= 2 ? k256 : k512;
+}
+
 bool plan_rows(int M, int N, int dtype, int epi, bool split_ok, int* mf, int* nf, int* ks) {
   *ks = 1;
-  if (epi == EPI_RESID && dtype == SD_DTYPE_BF16 && split_ok && M >= 128 && M <= 640 && N % 128 == 0) {
+  if (epi == EPI_RESID && dtype == SD_DTYPE_BF16 && split_ok && M >= 128 && M <= 640 && N % 128 == 0 &&
+      resid_ksplit(M, N) >= 2) {
     *mf = 4;
     *nf = 4;
-    *ks = 4;
+    *ks = resid_ksplit(M, N);
     return true;
   }
   if (epi == EPI_RESID && dtype == SD_DTYPE_BF16 && M >= 256 && M <= 640 && N % 64 == 0) {

@@ -208,6 +208,16 @@ def test_13b_width_largest_row_tiled_residual():
     _check(t, d, 1, 2, B=80, gamma=7, prompt_len=96, sample_tasks=[0, 79])
 
 
+@pytest.mark.parametrize("width,B,gamma,splits", [("13b", 32, 4, 6), ("13b", 64, 6, 3), ("7b", 64, 4, 5)])
+def test_residual_projection_k_splits(width, B, gamma, splits):
+    """Verify passes whose residual projections split K 6, 3 and 5 ways (160,
+    448 and 320 rows): the RMSNorm after them adds that many partial sums."""
+    t = synth.MODELS[f"{width}_target"].replace(n_layers=1)
+    d = synth.MODELS[f"{width}_draft"].replace(n_layers=1)
+    say("residual K split", splits)
+    _check(t, d, 1, 2, B=B, gamma=gamma, prompt_len=128, sample_tasks=[0, B - 1])
+
+
 def test_small_width_maximum_context():
     """One task at the largest context a slot takes (max_ctx 32768): a
     32750-token prompt, gamma = 4, 1-layer cuts of the small GQA pair."""
