@@ -193,7 +193,12 @@ int sd_init_static(const sd_config *cfg, const sd_weights *target,
  * prompt[:-1] (Section II-A, prefill stage; the target runs the same pass
  * over the prompt) and sets the slot's next input to the last prompt token.
  * Blocks until done.  SD_ESTATE if a slot is in use, SD_ENOMEM if a pool
- * is short. */
+ * is short.
+ * Resume: after sd_kv_commit the committed state of a task is its prompt
+ * plus the tokens emitted so far (both caches equal those of a fresh
+ * prefill of that sequence); prefilling prompt + emitted, in this or
+ * another context, and continuing with the uniforms of the following steps
+ * continues the run. */
 int sd_prefill(sd_ctx *ctx, int B, const int32_t *slots, const int32_t *tokens,
                const int32_t *lens, const int32_t *max_new, void *stream);
 

@@ -6,4 +6,4 @@ device memory and streams through PyTorch.
 """
 from ._lib import SDError, lib  # noqa: F401
 from .engine import (SDEngine, Batch, GPUModel, StepGraph, generate, generate_graph,  # noqa: F401
-                     emitted_tokens, accept_resample)
+                     emitted_tokens, accept_resample, resume_prompts)

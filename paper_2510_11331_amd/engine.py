@@ -370,3 +370,13 @@ def emitted_tokens(n_acc: np.ndarray, out_tok: np.ndarray) -> List[List[int]]:
             a = int(n_acc[s, b])
             res[b].extend(int(t) for t in out_tok[s, b, :a + 1])
     return res
+
+
+def resume_prompts(prompts: Sequence[np.ndarray], emitted: Sequence[Sequence[int]]) -> List[np.ndarray]:
+    """Checkpoint / resume.  After sd_kv_commit a task's whole state is its
+    prompt, the tokens emitted so far, its step count and its uniform stream
+    (uniforms are indexed by task and step).  Prefilling prompt + emitted
+    into a slot re-creates the committed caches; the run then continues with
+    the uniforms of the steps that follow."""
+    return [np.concatenate([np.asarray(p, dtype=np.int32), np.asarray(e, dtype=np.int32)])
+            for p, e in zip(prompts, emitted)]

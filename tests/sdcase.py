@@ -35,8 +35,9 @@ def top2_gap(z: np.ndarray) -> float:
 
 
 def run_gpu_steps(eng, slots, prompts, gamma, n_steps, seed, task_ids, max_new=None,
-                  keep_logits=False):
-    """Prefill, then n_steps SD steps of one batch on the current stream.
+                  keep_logits=False, first_step=0):
+    """Prefill, then n_steps SD steps of one batch on the current stream,
+    with the uniforms of steps first_step .. first_step + n_steps - 1.
     Returns (per-task emitted tokens, n_acc [n_steps, B], batch, logits
     [n_steps, B, gamma+1, V] or None)."""
     import torch
@@ -46,7 +47,7 @@ def run_gpu_steps(eng, slots, prompts, gamma, n_steps, seed, task_ids, max_new=N
     max_new = max_new or [n_steps * (gamma + 1)] * B
     eng.prefill(slots, prompts, max_new)
     b = eng.batch(slots, gamma)
-    u = uniforms_device(synth.uniform_table(seed, task_ids, n_steps, gamma))
+    u = uniforms_device(synth.uniform_table(seed, task_ids, first_step + n_steps, gamma)[first_step:])
     z = torch.empty(B, gamma + 1, eng.vocab, dtype=torch.float32, device="cuda") if keep_logits else None
     accs, outs, logs = [], [], []
     for n in range(n_steps):

@@ -56,6 +56,25 @@ def test_rollback_leaves_fresh_prefill():
     assert task.x0 == seq[-1]
 
 
+@pytest.mark.parametrize("tau,greedy", [(1.0, False), (0.05, False), (1.0, True)])
+def test_resume_from_prompt_plus_emitted_continues_the_run(tau, greedy):
+    """Checkpoint / resume: a task rebuilt from prompt + emitted tokens and
+    stepped with the uniforms of the later steps emits what the uninterrupted
+    task emits (the committed caches equal a fresh prefill, pinned above)."""
+    target, draft = pair("bf16", eps=0.5)
+    gamma, n1, n2 = 3, 6, 8
+    prompt = synth.prompts(1, 7, target.s.vocab, first_task=9)[0]
+    u = synth.uniform_table(44, [9], n1 + n2, gamma)[:, 0]
+    whole = sd.SDTask(target, draft, prompt)
+    ref = [whole.step(gamma, u[n], tau, greedy) for n in range(n1 + n2)]
+    first = sd.SDTask(target, draft, prompt)
+    part1 = [first.step(gamma, u[n], tau, greedy) for n in range(n1)]
+    resumed = sd.SDTask(target, draft, list(prompt) + first.emitted)
+    part2 = [resumed.step(gamma, u[n], tau, greedy) for n in range(n1, n1 + n2)]
+    assert part1 + part2 == ref
+    assert len({a for a, _ in ref}) >= 2 or greedy
+
+
 def test_draft_equal_to_target_always_accepts_when_sampling():
     target, _ = pair("fp32")
     gamma = 4
