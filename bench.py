@@ -379,8 +379,10 @@ def gateup_kernel_name(M: int, N: int) -> str:
         mtiles = -(-M // (32 * best))
         nf = 4 if N % 128 == 0 and mtiles * (N // 128) >= 128 else 2
         grid = mtiles * N // (32 * nf)
-        nb = (4 if 159 // (4 * best + 4 * nf) >= 4 else 3) if grid <= 256 else 2   # LDS stages
-        return f"gemm_rows_kernel<{best}, {nf}, 2, {nb}>"
+        waves = 8 if grid <= 256 and best != 8 else 4      # one workgroup per CU: 8 waves
+        spare = 1 if waves == 8 and (best % 2 or nf % 2) else 0
+        nb = (4 if 159 // (4 * best + 4 * nf + spare) >= 4 else 3) if grid <= 256 else 2   # LDS stages
+        return f"gemm_rows_kernel<{best}, {nf}, 2, {nb}, {waves}>"
     if M > 64:
         return "gemm_kernel<_Float16, 4, 2, 2, 2>"
     mt = -(-M // 16)

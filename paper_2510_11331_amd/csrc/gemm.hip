@@ -453,8 +453,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 // rows, so the operands are staged once per workgroup in LDS and shared.
 // A workgroup of 4 waves (2 x 2) owns a BM x BN = 32 MF x 32 NF output tile;
 // wave (wm, wn) owns the 16 MF x 16 NF sub-tile at (wm 16 MF, wn 16 NF).
+// With 8 waves (one workgroup per CU) waves w and w + 4 own the same
+// sub-tile and take the first and the second k-step of each stage; the
+// second adds its sums to the first's through LDS at the end.
 // K advances in stages of two k-steps (64 fp16); a stage is the
-// 2 (BM + BN) / 16 1 KB fragments, which the 4 waves load straight into
+// 2 (BM + BN) / 16 1 KB fragments, which the waves load straight into
 // one of NB LDS buffers (buffer loads with an LDS destination: lane i's
 // 16 bytes land at the buffer's fragment base + 16 i, no registers held).
 // NB - 1 stages are in flight while one is multiplied: at the top of stage
@@ -469,18 +472,22 @@ __device__ __forceinline__ void wait_vmcnt() {
 // loads).  Tile order: the row tiles of one column tile take consecutive
 // slots of one XCD (1-D grid, round-robin dispatch over 8 XCDs), so its
 // weights are fetched from HBM once and re-read from that XCD's L2.
-template <int MF, int NF, int EPI, int NB>
-__global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
+template <int MF, int NF, int EPI, int NB, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void gemm_rows_kernel(GemmParams p) {
   using T = f16_t;
+  static_assert(WAVES == 4 || WAVES == 8, "4 waves, or 8 that split each stage's two k-steps");
   constexpr int BM = 32 * MF, BN = 32 * NF;
-  constexpr int FA = 2 * BM / 16, FW = 2 * BN / 16, FS = FA + FW;   // fragments per stage
-  static_assert(NB >= 2 && (NB - 2) * (MF + NF) < 64, "stages in flight");
+  constexpr int FA = 2 * BM / 16, FW = 2 * BN / 16;   // fragments per stage
+  constexpr int LA = (FA + WAVES - 1) / WAVES, LW = (FW + WAVES - 1) / WAVES;   // loads per wave
+  constexpr int SPARE = (WAVES * LA > FA || WAVES * LW > FW) ? 1 : 0;          // their overflow slot
+  constexpr int FS = FA + FW + SPARE;
+  static_assert(NB >= 2 && (NB - 2) * (LA + LW) < 64, "stages in flight");
   extern __shared__ __align__(16) unsigned char smem[];
   u32x4* lds = (u32x4*)smem;                          // [NB][FS][64]
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave & 1, wn = (wave >> 1) & 1;
   const int r16 = lane & 15, g = lane >> 4;
   const int ksteps = p.K * 2 / 64, stages = ksteps / 2;
   const int gx = p.N / BN, gz = (p.M + BM - 1) / BM;
@@ -507,27 +514,31 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
   const __amdgpu_buffer_rsrc_t ar = buf_rsrc((const char*)p.A + (size_t)bz * (BM / 16) * tile_bytes, (BM / 16) * tile_bytes);
   const int mvalid = p.M - bz * BM;                   // rows of this tile below M
 
-  // this wave's share of stage st: A fragments f = 4 k + wave (k < MF), W
-  // fragments f = 4 k + wave (k < NF); fragment f = 2 t + u is (16-row tile
-  // t, k-step u of the stage)
+  // this wave's share of stage st: A fragments f = WAVES k + wave (k < LA), W
+  // fragments f = WAVES k + wave (k < LW); fragment f = 2 t + u is (16-row
+  // tile t, k-step u of the stage).  Indices past the stage's fragments load
+  // nothing (out-of-range offset) into the overflow slot, so every wave
+  // issues the same count
   auto gload = [&](int st) {
     const bool ok = st < s_hi;
     u32x4* base = lds + (size_t)(st % NB) * FS * 64;
 #pragma unroll
-    for (int k = 0; k < MF; ++k) {
-      const int f = 4 * k + wave, t = f >> 1, u = f & 1;
-      const uint32_t off = ok && 16 * t + r16 < mvalid
+    for (int k = 0; k < LA; ++k) {
+      const int f = WAVES * k + wave, t = f >> 1, u = f & 1;
+      const bool real = FA % WAVES == 0 || f < FA;       // known true when the loads divide evenly
+      const uint32_t off = real && ok && 16 * t + r16 < mvalid
                                ? (uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u
                                : OOB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ar, (__attribute__((address_space(3))) void*)(base + f * 64), 16, off,
-                                               0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ar, (__attribute__((address_space(3))) void*)(base + (real ? f : FA + FW) * 64),
+                                               16, off, 0, 0, 0);
     }
 #pragma unroll
-    for (int k = 0; k < NF; ++k) {
-      const int f = 4 * k + wave, t = f >> 1, u = f & 1;
-      const uint32_t off = ok ? (uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u : OOB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (__attribute__((address_space(3))) void*)(base + (FA + f) * 64), 16,
-                                               off, 0, 0, 0);
+    for (int k = 0; k < LW; ++k) {
+      const int f = WAVES * k + wave, t = f >> 1, u = f & 1;
+      const bool real = FW % WAVES == 0 || f < FW;
+      const uint32_t off = real && ok ? (uint32_t)t * tile_bytes + (uint32_t)(2 * st + u) * 1024u + lane * 16u : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (__attribute__((address_space(3))) void*)(base + (real ? FA + f : FA + FW) * 64),
+                                               16, off, 0, 0, 0);
     }
   };
 
@@ -540,12 +551,14 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
 #pragma unroll
   for (int st = 0; st < NB - 1; ++st) gload(s_lo + st);
   for (int st = s_lo; st < s_hi; ++st) {
-    wait_vmcnt<(NB - 2) * (MF + NF)>();
+    wait_vmcnt<(NB - 2) * (LA + LW)>();
     asm volatile("s_barrier" ::: "memory");
     gload(st + NB - 1);
     const u32x4* base = lds + (size_t)(st % NB) * FS * 64;
+    // 4 waves: both k-steps of the stage; 8 waves: wave group w / 4 takes k-step w / 4
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int uu = 0; uu < 8 / WAVES; ++uu) {
+      const int u = WAVES == 8 ? wave >> 2 : uu;
       u32x4 a[MF], b[NF];
 #pragma unroll
       for (int i = 0; i < MF; ++i) a[i] = base[(2 * (wm * MF + i) + u) * 64 + lane];
@@ -558,6 +571,28 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
     }
   }
   wait_vmcnt<0>();                                    // the trailing out-of-range loads
+  if constexpr (WAVES == 8) {
+    // waves 4-7 hand their k-step-1 sums to waves 0-3 through LDS (the stage
+    // buffers, free once every wave is past the loop); waves 0-3 then finish
+    float* red = (float*)smem + (size_t)(wave & 3) * MF * NF * 4 * 64;
+    __syncthreads();
+    if (wave >= 4) {
+#pragma unroll
+      for (int i = 0; i < MF; ++i)
+#pragma unroll
+        for (int j = 0; j < NF; ++j)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) red[((i * NF + j) * 4 + v) * 64 + lane] = acc[i][j][v];
+    }
+    __syncthreads();
+    if (wave >= 4) return;
+#pragma unroll
+    for (int i = 0; i < MF; ++i)
+#pragma unroll
+      for (int j = 0; j < NF; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[i][j][v] += red[((i * NF + j) * 4 + v) * 64 + lane];
+  }
 
   // epilogue: element (i, j, v) is row bz BM + wm 16 MF + 16 i + 4 g + v,
   // column n0 + 16 j + r16 with n0 the first column of the wave's sub-tile.
@@ -686,35 +721,59 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(GemmParams p) {
 // 65.0), QKV 55.3 -> 36.7, LM head 71.9 -> 59.1; 13B gate/up at M = 320
 // (432 workgroups) 118 -> 110 us with 2 stages (4: 124.6), LM head 125.5
 // -> 111.3 (4: 153.8).
-constexpr int rows_stage_kb(int mf, int nf) { return 4 * mf + 4 * nf; }
-constexpr int rows_stages_max(int mf, int nf) { return 159 / rows_stage_kb(mf, nf) >= 4 ? 4 : 3; }
-int gemm_rows_stages(int mf, int nf, int grid) { return grid <= 256 ? rows_stages_max(mf, nf) : 2; }
-size_t gemm_rows_lds(int mf, int nf, int nb) { return (size_t)nb * rows_stage_kb(mf, nf) * 1024; }
+// With at most 256 workgroups (one per CU) the kernel runs 8 waves: two per
+// SIMD issue the LDS fills and matrix instructions that one wave per SIMD
+// left half idle.  7B paged verify at M = 160 (kernel trace): gate/up 56.4
+// -> 54.4 us, O / down with K split 24.3 -> 22.9, LM head 62.8 -> 60.7;
+// above 256 workgroups two 4-wave workgroups share a CU instead.
+constexpr int rows_stage_kb(int mf, int nf, int waves) {
+  const int fa = 4 * mf, fw = 4 * nf, la = (fa + waves - 1) / waves, lw = (fw + waves - 1) / waves;
+  return fa + fw + ((waves * la > fa || waves * lw > fw) ? 1 : 0);
+}
+constexpr int rows_stages_max(int mf, int nf, int waves) {
+  return 159 / rows_stage_kb(mf, nf, waves) >= 4 ? 4 : 3;
+}
+constexpr bool rows_waves8(int epi, int mf) { return epi != EPI_RESID && epi != EPI_QKV && mf != 8; }
+int gemm_rows_stages(int mf, int nf, int grid, int epi) {
+  return grid <= 256 ? rows_stages_max(mf, nf, rows_waves8(epi, mf) ? 8 : 4) : 2;
+}
+size_t gemm_rows_lds(int mf, int nf, int nb, int waves) {
+  const size_t stages = (size_t)nb * rows_stage_kb(mf, nf, waves) * 1024;
+  const size_t red = waves == 8 ? (size_t)4 * mf * nf * 4 * 64 * sizeof(float) : 0;
+  return std::max(stages, red);
+}
 
-template <int EPI, int MF, int NF, int NB>
+template <int EPI, int MF, int NF, int NB, int WAVES>
 static hipError_t launch_rows_t(int gz, const GemmParams& p, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  const size_t lds = gemm_rows_lds(MF, NF, NB);
+  const size_t lds = gemm_rows_lds(MF, NF, NB, WAVES);
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_rows_kernel<MF, NF, EPI, NB>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_rows_kernel<MF, NF, EPI, NB, WAVES>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  launch_k(gemm_rows_kernel<MF, NF, EPI, NB>, dim3(p.N / (32 * NF) * gz * std::max(p.ksplit, 1)), dim3(256),
-           (uint32_t)lds, s, e0, e1, p);
+  launch_k(gemm_rows_kernel<MF, NF, EPI, NB, WAVES>, dim3(p.N / (32 * NF) * gz * std::max(p.ksplit, 1)),
+           dim3(64 * WAVES), (uint32_t)lds, s, e0, e1, p);
   return hipGetLastError();
 }
 
 template <int EPI>
 static hipError_t launch_rows_e(int mf, int nf, int gz, const GemmParams& p, hipStream_t s, hipEvent_t e0,
                                 hipEvent_t e1) {
-  const int nb = gemm_rows_stages(mf, nf, p.N / (32 * nf) * gz * std::max(p.ksplit, 1));
+  const int grid = p.N / (32 * nf) * gz * std::max(p.ksplit, 1);
+  const int nb = gemm_rows_stages(mf, nf, grid, EPI);
+  // the residual-add epilogue (a tile of residual values held), the QKV
+  // epilogue (the row positions, KV blocks and rotary inputs of all of a
+  // lane's rows prefetched) and 256-row tiles stay on 4 waves: 8 would leave
+  // them short of registers (QKV on 8 waves with a row-at-a-time epilogue:
+  // 7B at M = 160 50.2 us against 45.5)
 #define SD_ROWS_CASE(MFv, NFv)                                                            \
   if (mf == MFv && nf == NFv) {                                                           \
-    constexpr int hi = rows_stages_max(MFv, NFv);                                         \
-    return nb == 2 ? launch_rows_t<EPI, MFv, NFv, 2>(gz, p, s, e0, e1)                    \
-                   : launch_rows_t<EPI, MFv, NFv, hi>(gz, p, s, e0, e1);                  \
+    constexpr int w1 = rows_waves8(EPI, MFv) ? 8 : 4;                                     \
+    constexpr int hi = rows_stages_max(MFv, NFv, w1);                                     \
+    return nb == 2 ? launch_rows_t<EPI, MFv, NFv, 2, 4>(gz, p, s, e0, e1)                 \
+                   : launch_rows_t<EPI, MFv, NFv, hi, w1>(gz, p, s, e0, e1);              \
   }
   SD_ROWS_CASE(4, 2) SD_ROWS_CASE(5, 2) SD_ROWS_CASE(6, 2) SD_ROWS_CASE(8, 2)
   SD_ROWS_CASE(4, 4) SD_ROWS_CASE(5, 4) SD_ROWS_CASE(6, 4) SD_ROWS_CASE(8, 4)
