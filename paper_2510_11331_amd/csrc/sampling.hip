@@ -242,6 +242,7 @@ __global__ __launch_bounds__(RT) void draft_sample_kernel(DraftSampleParams p) {
   const int b = blockIdx.x, t = threadIdx.x;
   float4* q = (float4*)(p.q + ((size_t)b * p.gamma + p.i) * p.V);
   const int V4 = p.V >> 2;
+  const uint32_t ur = p.u[(size_t)b * (2 * p.gamma + 1) + p.i];   // loaded with the row, used by the draw
   float4 x[SV];
   load_strided(p.z + (size_t)b * p.V, p.V, x, -INFINITY);
   int tok;
@@ -270,7 +271,7 @@ __global__ __launch_bounds__(RT) void draft_sample_kernel(DraftSampleParams p) {
       x[k].x *= inv; x[k].y *= inv; x[k].z *= inv; x[k].w *= inv;
       if (t + RT * k < V4) q[t + RT * k] = x[k];
     }
-    tok = strided_sample(x, p.u[(size_t)b * (2 * p.gamma + 1) + p.i], pre, &total, &result);
+    tok = strided_sample(x, ur, pre, &total, &result);
     if (tok < 0) tok = 0;                       // no integer mass: impossible for a softmax row
   }
   if (t == 0) p.draft_tok[b * p.gamma + p.i] = tok;
@@ -300,24 +301,27 @@ __global__ __launch_bounds__(RT) void accept_kernel(AcceptParams p) {
       y = strided_argmax(w, red, redi);
     }
   } else {
-    if (threadIdx.x == 0) {
-      int aa = g;
-      for (int i = 0; i < g; ++i) {
-        const int t = dt[i];
-        bool ok = false;
-        if (t >= 0 && t < V) {
-          const float ui = (float)(u[g + i] >> 8) * 5.9604644775390625e-08f;   // * 2^-24, exact
-          ok = __fmul_rn(ui, q[(size_t)i * V + t]) < pp[(size_t)i * V + t];
-        } else if (p.err) {
-          atomicOr(p.err, ERR_BAD_TOKEN);
-        }
-        if (!ok) { aa = i; break; }
+    // the gamma ratio tests in parallel (lane i of wave 0 tests draft i, all
+    // loads in one round trip); a is the first failing test, as in the
+    // sequential rule, and only a bad token at position a is flagged (the
+    // positions before it were accepted, the ones after it never examined)
+    const uint32_t r = u[2 * g];
+    if (threadIdx.x < 64) {
+      const int i = threadIdx.x;
+      const int t = i < g ? dt[i] : 0;
+      const bool valid = i < g && t >= 0 && t < V;
+      bool ok = false;
+      if (valid) {
+        const float ui = (float)(u[g + i] >> 8) * 5.9604644775390625e-08f;   // * 2^-24, exact
+        ok = __fmul_rn(ui, q[(size_t)i * V + t]) < pp[(size_t)i * V + t];
       }
-      s_a = aa;
+      const uint64_t fail = __ballot(i < g && !ok);
+      const int aa = fail ? __ffsll((unsigned long long)fail) - 1 : g;
+      if (i == aa && i < g && !valid && p.err) atomicOr(p.err, ERR_BAD_TOKEN);
+      if (i == 0) s_a = aa;
     }
     __syncthreads();
     a = s_a;
-    const uint32_t r = u[2 * g];
     load_strided(pp + (size_t)a * V, V, w, 0.f);
     if (a < g) {
       const float* qa = q + (size_t)a * V;
