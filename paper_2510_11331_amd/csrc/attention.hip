@@ -117,7 +117,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
 
   int maxpos = -1;
   for (int r = 0; r < nr; ++r) maxpos = max(maxpos, p.row_pos[row0 + r]);
-  const int slot = p.row_slot[row0];
+  const int slot = p.row_bt ? 0 : p.row_slot[row0];   // decode passes: the row block's own table row
   const int k_begin = split * p.keys_per_split;
   // keys never extend past the slot's block-table row
   const int k_end = min(min(k_begin + p.keys_per_split, maxpos + 1), p.mbps * 16);
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnParams p) {
   for (int k = 0; k < QPT; ++k) o[k] = 0.f;
 
   const T* kv = (const T*)p.kv;
-  const int32_t* bt = p.block_table + (size_t)slot * p.mbps;
+  const int32_t* bt = (p.row_bt ? p.row_bt + (size_t)rb * p.mbps : p.block_table + (size_t)slot * p.mbps);
 
   for (int c = k_begin; c < k_end; c += 64) {
     __syncthreads();
@@ -296,14 +296,14 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(A
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) maxpos = max(maxpos, __shfl_xor(maxpos, o));
   maxpos = __builtin_amdgcn_readfirstlane(maxpos);
-  const int slot = p.row_slot[row0];
+  const int slot = p.row_bt ? 0 : p.row_slot[row0];   // decode passes: the row block's own table row
   const int k_begin = split * p.keys_per_split;
   const int k_end = min(min(k_begin + p.keys_per_split, maxpos + 1), p.mbps * 16);
 
   // block ids of the split's key range, staged in LDS (the host keeps a
   // split within ATTN_BT_CAP blocks): a key load then never waits on the
   // memory counter behind the keys still in flight
-  const int32_t* bt = p.block_table + (size_t)slot * p.mbps;
+  const int32_t* bt = (p.row_bt ? p.row_bt + (size_t)rb * p.mbps : p.block_table + (size_t)slot * p.mbps);
   const int bfirst = k_begin / 16, nbr = max(0, (k_end + 15) / 16 - bfirst);
   for (int i = tid; i < min(nbr, ATTN_BT_CAP); i += blockDim.x) s_bt[i] = bt[bfirst + i];
   __syncthreads();

@@ -131,6 +131,9 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsParams p) {
       }
       return;
     }
+    if (p.row_bt && j == 0)   // the task's block-table row, for this pass's attention
+      for (int i = threadIdx.x; i < p.mbps; i += 256)
+        p.row_bt[(size_t)b * p.mbps + i] = p.block_table[(size_t)slot * p.mbps + i];
     const int32_t* st = p.state + (size_t)slot * ST_N;
     const int P = st[ST_LEN];
     if (p.mode == ROWS_VERIFY) {

@@ -44,6 +44,7 @@ struct ModelRT {
 struct Lane {
   int rows = 0;                 // row capacity
   int32_t *row_tok = nullptr, *row_pos = nullptr, *row_slot = nullptr, *row_blk = nullptr, *rowblocks = nullptr;
+  int32_t* row_bt = nullptr;    // [decode row blocks, mbps] block-table rows of a decode pass's tasks
   int rb_cap = 0;
   float *x = nullptr, *q = nullptr, *logits = nullptr;
   void *xn = nullptr, *att = nullptr, *hmid = nullptr;
@@ -190,7 +191,7 @@ Dims dims_max(const sd_model_cfg& a, const sd_model_cfg* b) {
 
 // lane buffers; decode_rb = row blocks of a decode pass, qmax_dec = query vectors per row block
 void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int qmax_dec, int splits,
-              int logits_rows, int prefill_rb) {
+              int logits_rows, int prefill_rb, int mbps) {
   rows = (rows + GEMM_MROWS - 1) / GEMM_MROWS * GEMM_MROWS;   // operands are read in whole 64-row blocks
   ln.rows = rows;
   ln.row_tok = al.take<int32_t>(sizeof(int32_t) * rows);
@@ -199,6 +200,7 @@ void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int q
   ln.row_blk = al.take<int32_t>(sizeof(int32_t) * rows);
   ln.rb_cap = prefill_rb;
   ln.rowblocks = al.take<int32_t>(sizeof(int32_t) * 2 * std::max(1, prefill_rb));
+  ln.row_bt = al.take<int32_t>(sizeof(int32_t) * (size_t)decode_rb * mbps);
   ln.x = al.take<float>(sizeof(float) * rows * D.d);
   ln.xn = al.take<void>(D.esz * rows * D.d);
   ln.q = al.take<float>(sizeof(float) * rows * D.nq);
@@ -241,8 +243,8 @@ size_t layout(const sd_config* c, sd_ctx* ctx) {
   const int qb = std::min(prefill_qb(c->target), prefill_qb(c->draft));
   const int prefill_rb = c->prefill_rows / qb + c->max_slots + 1;
   Lane lv, ld;
-  lay_lane(al, lv, rows_v, Dt, c->max_batch, (c->gamma_max + 1) * Dt.G, splits, 0, prefill_rb);
-  lay_lane(al, ld, 2 * c->max_batch, Dd, c->max_batch, 2 * Dd.G, splits, c->max_batch, 0);
+  lay_lane(al, lv, rows_v, Dt, c->max_batch, (c->gamma_max + 1) * Dt.G, splits, 0, prefill_rb, mbps);
+  lay_lane(al, ld, 2 * c->max_batch, Dd, c->max_batch, 2 * Dd.G, splits, c->max_batch, 0, mbps);
   if (ctx) {
     ctx->mbps = mbps;
     ctx->state = state;
@@ -507,6 +509,7 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
   rows.row_blk = ln.row_blk;
   rows.block_table = bt;
   rows.mbps = ctx->mbps;
+  rows.row_bt = rowblocks ? nullptr : ln.row_bt;
   rows.state = ctx->state;
   rows.err = ctx->err;
   rows.n_slots = ctx->cfg.max_slots;
@@ -530,6 +533,7 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.q = ln.q;
     ap.kv = rp.kv;
     ap.block_table = bt;
+    ap.row_bt = rowblocks ? nullptr : ln.row_bt;
     ap.mbps = ctx->mbps;
     ap.nblk = m.n_blocks;
     ap.row_pos = ln.row_pos;

@@ -119,6 +119,8 @@ struct RowsParams {
   int32_t* row_blk;          // [M] KV block the row's K/V go to; -1 = none (inactive, or over capacity)
   const int32_t* block_table;  // [slots, mbps] of the model run over the rows
   int mbps;
+  int32_t* row_bt;           // null (prefill), or [B, mbps]: task b's block-table row, copied for the
+                             // attention of the pass (row block b), which then needs no slot lookup
   const void* embed;         // [V, d]
   const void* gain;          // [d]
   float* x;                  // [M, d]
@@ -171,6 +173,7 @@ struct AttnParams {
   const float* q;            // [M, H hd] (rotary applied)
   const void* kv;            // layer base of the pool (kv_tile_off)
   const int32_t* block_table;
+  const int32_t* row_bt;     // null, or [nrb, mbps]: row block rb's block-table row (decode passes)
   int mbps, nblk;            // block-table width, blocks in the pool
   const int32_t* row_pos;
   const int32_t* row_slot;
