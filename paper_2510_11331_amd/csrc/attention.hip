@@ -19,8 +19,10 @@
 // head and all rows of the block are one set of query vectors that shares
 // every K/V tile.  Query i only sees keys at positions <= its own.  Each work
 // item keeps an online softmax (running max, running sum, rescaled output);
-// when the keys are split, partial (max, sum, output) triples go to a
-// workspace and a second kernel merges them in split order.
+// when the keys are split (evenly over the item's context), partial (max,
+// sum, output) triples go to a workspace with device-scope stores, and the
+// last split of the item to finish merges them in split order (the fp32
+// kernel leaves the merge to a second kernel).
 //
 // bf16 models (fp16 KV cache, see f16_t): S^T = K Q^T and O^T += V^T P^T on
 // v_mfma_f32_16x16x32_f16, 16 query vectors per wave, keys streamed from the
@@ -297,8 +299,13 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(A
   for (int o = 32; o > 0; o >>= 1) maxpos = max(maxpos, __shfl_xor(maxpos, o));
   maxpos = __builtin_amdgcn_readfirstlane(maxpos);
   const int slot = p.row_bt ? 0 : p.row_slot[row0];   // decode passes: the row block's own table row
-  const int k_begin = split * p.keys_per_split;
-  const int k_end = min(min(k_begin + p.keys_per_split, maxpos + 1), p.mbps * 16);
+  // the item's keys (positions 0 .. maxpos) are dealt out evenly over the
+  // splits in 32-key steps, at most the host's keys_per_split per split
+  // (which bounds the staged block ids)
+  const int kps = p.splits > 1 ? min(p.keys_per_split, ((maxpos + p.splits) / p.splits + 31) / 32 * 32)
+                               : p.keys_per_split;
+  const int k_begin = split * kps;
+  const int k_end = min(min(k_begin + kps, maxpos + 1), p.mbps * 16);
 
   // block ids of the split's key range, staged in LDS (the host keeps a
   // split within ATTN_BT_CAP blocks): a key load then never waits on the
@@ -499,24 +506,84 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(A
     return;
   }
 
-  // key split: partial (output, max, sum) for attn_merge_kernel
-  const size_t item = ((size_t)rbk * p.splits + split) * p.qmax + (owner ? qi : 0);
+  // key split: this workgroup's partial (output, max, sum) goes out with
+  // device-scope stores; the item's last split to finish merges them
+  const size_t base = (size_t)rbk * p.splits * p.qmax;
+  const size_t item = base + (size_t)split * p.qmax + (owner ? qi : 0);
   if (owner) {
 #pragma unroll
     for (int d = 0; d < DT; ++d)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) p.part_o[item * HD + 16 * d + 4 * g + v] = o[d][v];
+      for (int v = 0; v < 4; ++v)
+        __hip_atomic_store(p.part_o + item * HD + 16 * d + 4 * g + v, o[d][v], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     if (g == 0) {
-      p.part_ml[item * 2] = m_run == -INFINITY ? -INFINITY : m_run * 0.6931471805599453f;   // natural units for the merge
-      p.part_ml[item * 2 + 1] = l_run;
+      // natural units for the merge
+      __hip_atomic_store(p.part_ml + item * 2, m_run == -INFINITY ? -INFINITY : m_run * 0.6931471805599453f,
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.part_ml + item * 2 + 1, l_run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+  }
+  __shared__ int s_last;
+  __builtin_amdgcn_s_waitcnt(0);      // this wave's partial stores have reached device scope
+  __syncthreads();
+  if (tid == 0) {
+    const int old = __hip_atomic_fetch_add(p.cnt + rbk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = old == p.splits - 1;
+    if (last) __hip_atomic_store(p.cnt + rbk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = last;
+  }
+  __syncthreads();
+  if (!s_last) return;
+
+  // merge, in split order: O = sum_s o_s e^(m_s - M) / sum_s l_s e^(m_s - M),
+  // M = max_s m_s; every load of a query's splits is issued before any is used
+  __shared__ float s_w[ATTN_QMAX][ATTN_MAX_SPLITS], s_L[ATTN_QMAX];
+  for (int qj = tid; qj < Qn; qj += 64 * WAVES) {
+    float ms[ATTN_MAX_SPLITS], ls[ATTN_MAX_SPLITS];
+#pragma unroll
+    for (int sp = 0; sp < ATTN_MAX_SPLITS; ++sp) {
+      const size_t it = (base + (size_t)sp * p.qmax + qj) * 2;
+      ms[sp] = sp < p.splits ? __hip_atomic_load(p.part_ml + it, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                             : -INFINITY;
+      ls[sp] = sp < p.splits ? __hip_atomic_load(p.part_ml + it + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                             : 0.f;
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < ATTN_MAX_SPLITS; ++sp) M = fmaxf(M, ms[sp]);
+    float L = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < ATTN_MAX_SPLITS; ++sp) {
+      const float w = ms[sp] == -INFINITY ? 0.f : expf(ms[sp] - M);
+      L += ls[sp] * w;
+      s_w[qj][sp] = w;
+    }
+    s_L[qj] = L;
+  }
+  __syncthreads();
+  for (int idx = tid; idx < Qn * HD; idx += 64 * WAVES) {
+    const int qj = idx / HD, d = idx % HD;
+    float os[ATTN_MAX_SPLITS];
+#pragma unroll
+    for (int sp = 0; sp < ATTN_MAX_SPLITS; ++sp)
+      os[sp] = sp < p.splits ? __hip_atomic_load(p.part_o + (base + (size_t)sp * p.qmax + qj) * HD + d,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                             : 0.f;
+    float O = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < ATTN_MAX_SPLITS; ++sp) O += os[sp] * s_w[qj][sp];
+    const float L = s_L[qj];
+    const int row = row0 + qj / G, h = kvh * G + qj % G;
+    Store<f16_t>::store((f16_t*)p.out, Tile<f16_t>::off(row, h * HD + d, p.H * HD), L > 0.f ? O / L : 0.f);
   }
 }
 
-// Merge of the key splits of every (row block, kv head) item, in split order:
-// O = sum_s o_s e^(m_s - M) / sum_s l_s e^(m_s - M), M = max_s m_s.  A second
-// kernel instead of a last-arriving workgroup: on MI355X a device-scope
-// release per workgroup costs more than a kernel boundary.
+// Merge of the key splits of every (row block, kv head) item of the fp32
+// kernel, in split order: O = sum_s o_s e^(m_s - M) / sum_s l_s e^(m_s - M),
+// M = max_s m_s.  (The matrix kernel merges its splits itself: the last split
+// of an item to finish reads the others' partials, written with device-scope
+// stores, and no L2 write-back or second launch is needed.)
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   const int rbk = blockIdx.x, rb = rbk / p.KV, kvh = rbk % p.KV;
@@ -581,8 +648,9 @@ hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEv
   if (p.keys_per_split % 64 || p.keys_per_split > ATTN_BT_CAP * 16) return hipErrorInvalidValue;
   const dim3 grid(p.nrb * p.KV, p.splits);
   if (dtype == 0) {
-    const bool split = p.splits > 1;
-    hipEvent_t e1a = split ? nullptr : e1;
+    // a split item's last workgroup merges: every split needs the counter, and
+    // the merge holds at most ATTN_MAX_SPLITS partials per query
+    if (p.splits > 1 && (!p.cnt || p.splits > ATTN_MAX_SPLITS)) return hipErrorInvalidValue;
     // four waves per workgroup for large grids (hd 64: 1024 or more
     // workgroups, hd 128: 2048): two then share a CU, and one's start and
     // merge overlap the other's stream.  13B B = 64 (2560 verify and 1024
@@ -590,13 +658,11 @@ hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEv
     // verify workgroups) is 0.7 % slower with four, so keeps eight
     const bool many = grid.x * grid.y >= (p.hd == 64 ? 1024u : 2048u);
     if (p.hd == 64) {
-      if (many) launch_k(attention_mfma_kernel<64, 4>, grid, dim3(64 * 4), 0, s, e0, e1a, p);
-      else launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
-      if (split) launch_k(attn_merge_kernel<f16_t, 64>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
+      if (many) launch_k(attention_mfma_kernel<64, 4>, grid, dim3(64 * 4), 0, s, e0, e1, p);
+      else launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1, p);
     } else if (p.hd == 128) {
-      if (many) launch_k(attention_mfma_kernel<128, 4>, grid, dim3(64 * 4), 0, s, e0, e1a, p);
-      else launch_k(attention_mfma_kernel<128, 8>, grid, dim3(64 * 8), 0, s, e0, e1a, p);
-      if (split) launch_k(attn_merge_kernel<f16_t, 128>, dim3(p.nrb * p.KV), dim3(256), 0, s, nullptr, e1, p);
+      if (many) launch_k(attention_mfma_kernel<128, 4>, grid, dim3(64 * 4), 0, s, e0, e1, p);
+      else launch_k(attention_mfma_kernel<128, 8>, grid, dim3(64 * 8), 0, s, e0, e1, p);
     } else {
       return hipErrorInvalidValue;
     }

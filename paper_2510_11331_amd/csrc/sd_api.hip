@@ -51,6 +51,7 @@ struct Lane {
   float* part = nullptr;        // [MAX_KSPLIT, part_rows, d] K-split partial sums
   int part_rows = 0;
   float *attn_o = nullptr, *attn_ml = nullptr;
+  int32_t* attn_cnt = nullptr;  // [attn_items] split arrival counters (zero between launches)
   size_t attn_o_cap = 0, attn_ml_cap = 0;
   int attn_items = 0;           // (row block, kv head) items the split partials hold
 };
@@ -214,6 +215,7 @@ void lay_lane(Alloc& al, Lane& ln, int rows, const Dims& D, int decode_rb, int q
   ln.attn_ml_cap = (size_t)ln.attn_items * splits * qmax_dec * 2;
   ln.attn_o = al.take<float>(sizeof(float) * ln.attn_o_cap);
   ln.attn_ml = al.take<float>(sizeof(float) * ln.attn_ml_cap);
+  ln.attn_cnt = al.take<int32_t>(sizeof(int32_t) * std::max(1, ln.attn_items));
 }
 
 // prefill rows per attention row block: as many as fit the 64 query vectors
@@ -318,10 +320,12 @@ struct GemmPlan {
 //     column pairs (fewer activation re-reads), else 32-column;
 //   * residual projections (O, down) with an RMSNorm after them (split_ok)
 //     and one row block: K split over workgroups until there are ~256 of
-//     them, 32-column tiles when every wave still gets >= 4 step groups,
-//     else 16-column; the partial sums go through the workspace to the
-//     RMSNorm, which adds them to the residual stream.  Without split_ok the
-//     output is added in place;
+//     them, 32-column tiles when every wave still gets >= 4 step groups
+//     (64-column for a single 16-row tile: four times fewer activation
+//     loads per weight load; 7B B = 1 verify pass 3.55 -> 3.20 ms, against
+//     3.24 with 32 columns), else 16-column; the partial sums go through the
+//     workspace to the RMSNorm, which adds them to the residual stream.
+//     Without split_ok the output is added in place;
 //   * LM head and other stores: 64-column tiles for 3-tile row blocks, else
 //     32-column (4-tile row blocks take at most 32 columns);
 //   * several 64-row blocks (B >= 32 verify, prefill): 32-column tiles.
@@ -358,7 +362,8 @@ GemmPlan plan_gemm(int M, int N, int K, size_t esz, int epi, bool split_ok = fal
       return std::min(std::min(SKINNY_MAX_KSPLIT, std::max(1, (256 + gx - 1) / gx)), std::max(1, groups / 4));
     };
     g.nt = 1;
-    if (g.mt >= 2 && pick(2) && groups / splits(2) >= 4 * g.kw) g.nt = 2;
+    if (pick(2) && groups / splits(2) >= 4 * g.kw) g.nt = 2;
+    if (g.mt == 1 && pick(4) && groups / splits(4) >= 4 * g.kw) g.nt = 4;
     g.ksplit = splits(g.nt);
   } else if (g.mt == 3 && pick(4)) {
     g.nt = 4;
@@ -545,11 +550,15 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.KV = c.n_kv_heads;
     ap.hd = c.head_dim;
     // split the keys when the (row block, kv head) items leave more than half
-    // of the 256 compute units idle; the splits are merged by a second kernel
+    // of the 256 compute units idle, into at most as many splits as keep the
+    // grid within one workgroup per CU (every split has keys to read: a
+    // second round of workgroups would double the pass); the last split of
+    // an item to finish merges them (16-bit caches), or a second kernel
+    // does (fp32)
     int splits = attn_splits;
     const int items = nrb * c.n_kv_heads;
-    if (items >= 128) splits = 1;
-    else if (splits > 1) splits = std::min(splits, std::max(1, (256 + items - 1) / items));
+    if (items >= ATTN_SPLIT_BELOW) splits = 1;
+    else if (splits > 1) splits = std::min(splits, std::max(1, 256 / items));
     const int kps = (ctx->cfg.max_ctx + 63) / 64 * 64;
     ap.splits = splits;
     ap.keys_per_split = splits > 1 ? std::max(ctx->keys_per_split, (kps / splits + 63) / 64 * 64) : kps;
@@ -558,7 +567,10 @@ int forward(sd_ctx* ctx, ModelRT& m, Lane& ln, RowsParams rows, int M, int nrb, 
     ap.out = ln.att;
     ap.part_o = ln.attn_o;
     ap.part_ml = ln.attn_ml;
+    ap.cnt = ln.attn_cnt;
     ap.qmax = qmax;
+    if (ap.splits > 1 && (items > ln.attn_items || (size_t)items * ap.splits * qmax * c.head_dim > ln.attn_o_cap))
+      return SD_EINVAL;   // the lane holds the partials of its decode passes only
     ProfRec ra;
     prof_begin(ctx, s, ra, verify ? SD_PROF_ATTN_VERIFY : -1, -1, 0, true);
     HIPCHK(launch_attention(dt, ap, s, ra.a, ra.b));

@@ -185,6 +185,7 @@ struct AttnParams {
   float* part_o;             // [nrb*KV, splits, Qmax, hd]
   float* part_ml;            // [nrb*KV, splits, Qmax, 2]
   int qmax;                  // max query vectors per (rowblock, kv head)
+  int* cnt;                  // [nrb*KV] arrivals of an item's key splits (16-bit caches; zero between launches)
 };
 
 struct SoftmaxParams {
@@ -285,6 +286,8 @@ constexpr int GEMM_MROWS = 64;         // rows per M block (4 MFMA row tiles)
 constexpr int ATTN_KEYS = 64;          // keys per LDS chunk
 constexpr int ATTN_QMAX = 64;          // max query vectors per workgroup
 constexpr int ATTN_BT_CAP = 2048;      // KV blocks of one key range staged in LDS (32768 positions)
+constexpr int ATTN_MAX_SPLITS = 12;    // key splits per item the matrix kernel merges itself
+constexpr int ATTN_SPLIT_BELOW = 128;  // decode passes with fewer (row block, kv head) items split the keys
 constexpr int MAX_CTX = ATTN_BT_CAP * 16;   // positions a slot may reach
 
 }  // namespace sd
