@@ -507,7 +507,12 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attention_mfma_kernel(A
   }
 
   // key split: this workgroup's partial (output, max, sum) goes out with
-  // device-scope stores; the item's last split to finish merges them
+  // device-scope stores; the item's last split to finish merges them.  Every
+  // value handed over is written and read with device-scope atomic
+  // operations, which the L2 of another XCD does not serve stale, so waiting
+  // for the stores before counting is all the ordering needed (a release /
+  // acquire fence would also write back and invalidate the whole L2, which
+  // only data written with plain stores needs)
   const size_t base = (size_t)rbk * p.splits * p.qmax;
   const size_t item = base + (size_t)split * p.qmax + (owner ? qi : 0);
   if (owner) {
