@@ -411,13 +411,15 @@ int resid_ksplit(int M, int N) {
   return g > 256 && g < 448 && k256 >= 2 ? k256 : k512;
 }
 
-bool plan_rows(int M, int N, int dtype, int epi, bool split_ok, int* mf, int* nf, int* ks) {
+bool plan_rows(int M, int N, int K, int dtype, int epi, bool split_ok, int* mf, int* nf, int* ks) {
   *ks = 1;
+  // a split range holds at least one stage (GEMM_CHUNK bytes of K)
+  const int ks_res = std::min(resid_ksplit(M, N), K * 2 / GEMM_CHUNK);
   if (epi == EPI_RESID && dtype == SD_DTYPE_BF16 && split_ok && M >= 128 && M <= 640 && N % 128 == 0 &&
-      resid_ksplit(M, N) >= 2) {
+      ks_res >= 2) {
     *mf = 4;
     *nf = 4;
-    *ks = resid_ksplit(M, N);
+    *ks = ks_res;
     return true;
   }
   if (epi == EPI_RESID && dtype == SD_DTYPE_BF16 && M >= 256 && M <= 640 && N % 64 == 0) {
@@ -453,7 +455,7 @@ int gemm(sd_ctx* ctx, const ModelRT& m, int epi, const void* A, const void* W, i
          float* out, int ldo, void* out_t, hipStream_t s, int prof_kind, int prof_kind2,
          const RopeParams* rope = nullptr, float* part = nullptr, int* nsplit = nullptr) {
   int mf = 0, nf = 0, rks = 1;
-  const bool rows = plan_rows(M, N, m.c.dtype, epi, part != nullptr, &mf, &nf, &rks);
+  const bool rows = plan_rows(M, N, K, m.c.dtype, epi, part != nullptr, &mf, &nf, &rks);
   GemmPlan g = plan_gemm(M, N, K, m.esz, epi, part != nullptr && !rows);
   if (!rows && !g.tu && N % (16 * g.nt)) return SD_EINVAL;
   const int ksplit = rows ? rks : g.ksplit;
