@@ -660,8 +660,11 @@ hipError_t launch_attention(int dtype, const AttnParams& p, hipStream_t s, hipEv
     // workgroups, hd 128: 2048): two then share a CU, and one's start and
     // merge overlap the other's stream.  13B B = 64 (2560 verify and 1024
     // draft workgroups): step 19.73 -> 18.38 ms; 7B paged B = 32 (1024
-    // verify workgroups) is 0.7 % slower with four, so keeps eight
-    const bool many = grid.x * grid.y >= (p.hd == 64 ? 1024u : 2048u);
+    // verify workgroups) is 0.7 % slower with four, so keeps eight.  Split
+    // hd 128 items (7B B = 1: a few hundred keys per split) also take four:
+    // a two-round key-group merge instead of three, 14.2 -> 13.9 us per
+    // layer (with twice the splits on them, 14.8)
+    const bool many = grid.x * grid.y >= (p.hd == 64 ? 1024u : 2048u) || (p.hd == 128 && p.splits > 1);
     if (p.hd == 64) {
       if (many) launch_k(attention_mfma_kernel<64, 4>, grid, dim3(64 * 4), 0, s, e0, e1, p);
       else launch_k(attention_mfma_kernel<64, 8>, grid, dim3(64 * 8), 0, s, e0, e1, p);
