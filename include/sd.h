@@ -163,7 +163,10 @@ size_t sd_kv_pool_bytes(const sd_config *cfg, int draft);
 size_t sd_workspace_bytes(const sd_config *cfg);
 
 /* Validate cfg, borrow the buffers, clear the workspace's device state.
- * On success *out holds a new context. */
+ * On success *out holds a new context.  The workspace then belongs to the
+ * context until sd_destroy: besides scratch it holds slot state and the
+ * attention's key-split counters, which every launch leaves at zero, so the
+ * caller must not write to it. */
 int sd_init(const sd_config *cfg, const sd_weights *target,
             const sd_weights *draft, sd_ctx **out);
 
